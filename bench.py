@@ -1,0 +1,270 @@
+"""Benchmark of the StateKV per-frame video-prefill step on one MI355X.
+
+A step is one frame of the video through every layer of the stack (attention
+with fused importance scoring, Top-B selection, state update, decode-cache
+append), in one skv_frame_step call.  The whole 512-frame video's Q/K/V are
+generated on the device and resident in HBM before timing; after the last
+frame the stream restarts from frame 0 with an empty state (skv_reset).
+
+Reported: frames/s over the K timed frames (host wall clock between two
+device synchronisations), per-stage kernel times from HIP events recorded on
+the library's stream, the attention kernel's roofline position, per-frame
+latency against frame index, and the fp64 CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "video-prefill frames/s (7B shape, 512 frames); % bf16 MFMA peak; HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+ATTN_SOURCES = ["paper_2605_31598_amd/csrc/attn_mfma.hip", "paper_2605_31598_amd/csrc/internal.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_mfma_vlm7b_28layer_traffic.txt")
+
+
+def attn_source_hash():
+    h = hashlib.sha256()
+    for p in ATTN_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic():
+    """HBM bytes per attention launch from the committed rocprofv3 counter summary,
+    valid only while the attention source is unchanged since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("attn_source_sha256_16") != attn_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def attention_flops(wl, S):
+    """Causal-exact algorithmic FLOPs of one frame over all layers: QK^T and PV once."""
+    T = wl.tokens_per_frame
+    return 4 * wl.head_dim * wl.n_q_heads * (T * S + T * (T + 1) // 2) * wl.n_layers
+
+
+def executed_mfma_flops(wl, S):
+    """MFMA FLOPs the kernel issues: two sweeps of K Q^T plus one V^T P^T over whole tiles
+    (64-row waves, 64-key tiles)."""
+    rows = wl.group * wl.tokens_per_frame
+    waves = -(-rows // 64)
+    keys = -(-(S + wl.tokens_per_frame) // 64) * 64
+    return 3 * 2 * (waves * 64) * keys * wl.head_dim * wl.n_kv_heads * wl.n_layers
+
+
+def stage_bytes(wl, S, n_qtiles):
+    """Algorithmic HBM bytes per launch of the select, update and append stages."""
+    LH = wl.n_layers * wl.n_kv_heads
+    T, rb = wl.tokens_per_frame, wl.head_dim * 2
+    P = S + T
+    select = LH * (n_qtiles * P * 4 + S * 4 + P * 8 + 2 * T * 4 + S * 4)
+    update_worst = LH * min(T, wl.capacity) * (2 * 2 * rb + 8)  # admitted rows: read + write K and V
+    append = LH * T * rb * 2 * 2
+    return select, update_worst, append
+
+
+def cpu_baseline(wl, seconds):
+    """The fp64 oracle on a bounded sample: layer 0, frames from state-full onward, on a
+    full state of the most recent tokens; scaled to frames/s of the whole stack."""
+    from oracle import statekv_oracle as orc
+    from workloads import generate as gen
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    n0 = wl.full_from_frame + 1
+    # state: most recent B tokens entering frame n0
+    S = wl.state_size(n0)
+    ks, vs, ps = [], [], []
+    for f in range(max(0, n0 - (-(-S // wl.tokens_per_frame))), n0):
+        x = gen.frame_inputs(wl, 0, f)
+        ks.append(gen.to_f64(x["k"], wl.dtype))
+        vs.append(gen.to_f64(x["v"], wl.dtype))
+        ps.append(orc.frame_positions(f, wl.tokens_per_frame, wl.pos_offset))
+    H = wl.n_kv_heads
+    st = orc.LayerState(np.tile(np.concatenate(ps)[-S:], (H, 1)), np.concatenate(ks, axis=1)[:, -S:],
+                        np.concatenate(vs, axis=1)[:, -S:], np.zeros((H, S)))
+    times = []
+    t_start = time.perf_counter()
+    n = n0
+    while time.perf_counter() - t_start < seconds and n < wl.n_frames:
+        x = gen.frame_inputs_f64(wl, 0, n)
+        t0 = time.perf_counter()
+        r = orc.frame_step(st, x["q"], x["k"], x["v"], n, wl.capacity, wl.scale, wl.pos_offset)
+        times.append(time.perf_counter() - t0)
+        st = r.state
+        n += 1
+    per_layer_frame = float(np.mean(times))
+    return {
+        "value": 1.0 / (per_layer_frame * wl.n_layers),
+        "unit": "frames/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"fp64 numpy oracle, layer 0 of {wl.n_layers}, frames {n0}..{n - 1} on a full state "
+                  f"({len(times)} layer-frames, {per_layer_frame * 1e3:.1f} ms each; input generation excluded); "
+                  f"scaled by {wl.n_layers} layers",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1536, help="timed frames (the video restarts after its last frame)")
+    ap.add_argument("--warmup", type=int, default=512, help="untimed frames before timing")
+    ap.add_argument("--workload", default="vlm7b_28layer")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (the step shards by KV head "
+              "and by layer with no exchange; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2605_31598_amd import FrameStepper
+    from workloads import CONFIGS
+    from workloads import device as wdev
+    from workloads import generate as gen
+
+    wl = CONFIGS[args.workload]
+    if wl.dtype != "bf16":
+        raise SystemExit("the benchmark runs bf16 workloads")
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    L, N, Hq, Hkv, T, d = wl.n_layers, wl.n_frames, wl.n_q_heads, wl.n_kv_heads, wl.tokens_per_frame, wl.head_dim
+
+    # whole video resident in HBM, generated on the device (untimed)
+    q_all = torch.empty((N, L, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    k_all = torch.empty((N, L, Hkv, T, d), dtype=torch.bfloat16, device="cuda")
+    v_all = torch.empty((N, L, Hkv, T, d), dtype=torch.bfloat16, device="cuda")
+    for t, tid in ((q_all, gen.TENSOR_Q), (k_all, gen.TENSOR_K), (v_all, gen.TENSOR_V)):
+        keys = [gen.stream_key(wl.seed, l, f, tid) for f in range(N) for l in range(L)]
+        wdev.fill_iid(t, keys, "bf16")
+    out = torch.empty((L, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    print(f"[bench] {wl.name}: inputs resident ({(q_all.numel() + k_all.numel() + v_all.numel()) * 2 / 1e9:.1f} GB)",
+          file=sys.stderr, flush=True)
+
+    st = FrameStepper.from_workload(wl, stream=stream)
+    counter = {"i": 0}
+
+    def run(n_frames):
+        for _ in range(n_frames):
+            f = counter["i"] % N
+            if f == 0 and counter["i"] > 0:
+                st.reset()
+            st.step(q_all[f], k_all[f], v_all[f], out)
+            counter["i"] += 1
+
+    run(args.warmup)
+    torch.cuda.synchronize()
+    first_frame = counter["i"] % N
+    st.timing_start(args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(args.steps)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stages = st.timing_stop(args.steps)  # [K, 4] ms
+    st.close()
+    elapsed = t1 - t0
+    fps = args.steps / elapsed
+    print(f"[bench] timed {args.steps} frames in {elapsed:.3f} s", file=sys.stderr, flush=True)
+
+    frames = (first_frame + np.arange(args.steps)) % N
+    S = np.minimum(wl.capacity, frames * T)
+    attn_ms = stages[:, 0].astype(np.float64)
+    alg = np.array([attention_flops(wl, int(s)) for s in S], dtype=np.float64)
+    exe = np.array([executed_mfma_flops(wl, int(s)) for s in S], dtype=np.float64)
+    achieved = alg.sum() / (attn_ms.sum() * 1e-3) / 1e12
+    executed = exe.sum() / (attn_ms.sum() * 1e-3) / 1e12
+    n_qtiles = -(-(wl.group * T) // 256)
+    sel_b, upd_b, app_b = (np.array([stage_bytes(wl, int(s), n_qtiles)[i] for s in S]) for i in range(3))
+
+    def gbs(b, col):
+        return float(b.sum() / (stages[:, col].astype(np.float64).sum() * 1e-3) / 1e9)
+
+    frame_ms = stages.sum(axis=1)
+    full = frames >= wl.full_from_frame
+    per_index = {}
+    for f, ms in zip(frames[full], frame_ms[full]):
+        per_index.setdefault(int(f), []).append(float(ms))
+    med_by_frame = np.array([np.median(v) for _, v in sorted(per_index.items())]) if per_index else np.array([0.0])
+    med = float(np.median(med_by_frame))
+    traffic = stored_traffic()
+
+    result = {
+        "metric": METRIC,
+        "value": round(fps, 3),
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * elapsed / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                   "tokens_per_frame": T, "frames_per_video": N, "capacity": wl.capacity,
+                   "layers_per_call": L, "inputs": "i.i.d. N(0,1) bf16, generated in HBM"},
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "kernel": "attn_mfma_kernel<128>",
+            "flops_per_launch": float(alg.mean()),
+            "avg_launch_ms": float(attn_ms.mean()),
+            "executed_mfma_tflops": round(executed, 2),
+            "executed_frac": round(executed / PEAK_BF16_TFLOPS, 4),
+        },
+        "stages_ms_mean": {n: float(stages[:, i].mean()) for i, n in enumerate(("attention", "select", "update",
+                                                                                  "append"))},
+        "hbm": {
+            "select_GBps": round(gbs(sel_b, 1), 1),
+            "update_GBps_at_T_admitted": round(gbs(upd_b, 2), 1),
+            "append_GBps": round(gbs(app_b, 3), 1),
+            "peak_GBps": PEAK_HBM_GBS,
+        },
+        "latency": {
+            "frame_ms_median_state_full": round(med, 4),
+            "flatness_max_dev": round(float(np.max(np.abs(med_by_frame / med - 1.0))), 4) if med > 0 else None,
+            "frame_ms_first_frames": [round(float(x), 4) for x in frame_ms[:min(16, len(frame_ms))]],
+            "from_frame": int(wl.full_from_frame),
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

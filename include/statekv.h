@@ -1,0 +1,162 @@
+/*
+ * statekv.h — C ABI of the StateKV per-frame streaming video-prefill step on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Linear Scaling Video VLMs for Long Video Understanding" (StateKV).
+ * For every layer, the T query tokens of frame n attend over the layer's
+ * compressed state C_{n-1} (capacity B, the only cross-frame context, Eq. 4)
+ * followed by the frame's own keys, causal inside the frame (Eq. 5, mask M_n).
+ * The same pass sums, for every candidate key, the attention mass it receives
+ * from the frame's queries of all query heads sharing its KV head, divided by
+ * T (the score instantiation of the "attention-driven selection" paragraph).
+ * The B best candidates (ties: lowest position) become C_n (Eq. 6); the frame's
+ * K/V rows are appended to the per-layer decode cache D (Eq. 4, the detailed
+ * state), which prefill never reads.  Token positions derive from the virtual
+ * length L_n (virtual sequence length paragraph).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers named q, k, v, out are DEVICE pointers owned by the caller.
+ * - Every device operation is enqueued on the HIP stream given to skv_init and
+ *   is stream-ordered; no call blocks the host except skv_timing_stop.
+ * - Errors are returned as skv_status; on error nothing is enqueued and the
+ *   context is unchanged.  Asynchronous device faults surface at the caller's
+ *   next synchronisation.
+ * - All device memory of a context is allocated once in skv_init and released
+ *   in skv_destroy; skv_frame_step allocates nothing.
+ * - A context is not thread-safe: calls on one context must be serialised.
+ */
+#ifndef STATEKV_H
+#define STATEKV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SKV_OK = 0,
+  SKV_ERR_INVALID_ARG = -1,   /* null pointer, bad size, unsupported combination */
+  SKV_ERR_OUT_OF_MEMORY = -2, /* device allocation failed in skv_init */
+  SKV_ERR_CAPACITY = -3,      /* decode cache full: frame >= max_frames */
+  SKV_ERR_ORDER = -4,         /* layer_begin is not the next layer of the current frame */
+  SKV_ERR_DEVICE = -5,        /* HIP runtime or launch error */
+  SKV_ERR_UNSUPPORTED = -6    /* valid request the library does not implement */
+} skv_status;
+
+typedef enum { SKV_BF16 = 0, SKV_F32 = 1 } skv_dtype;
+
+/* Problem statement of the method: head counts and head dimension d_h (Eq. 5),
+ * T tokens per frame, capacity B of the compressed state (Eq. 4), layer count,
+ * and the decode-cache length, which grows by T per frame. */
+typedef struct {
+  int32_t n_layers;         /* L >= 1 */
+  int32_t n_q_heads;        /* H_q, a multiple of n_kv_heads (grouped-query attention) */
+  int32_t n_kv_heads;       /* H_kv >= 1; query head h reads KV head h / (H_q / H_kv) */
+  int32_t head_dim;         /* d_h: 64 or 128 */
+  int32_t tokens_per_frame; /* T >= 1 */
+  int32_t capacity;         /* B >= 0 */
+  int32_t max_frames;       /* frames the decode cache holds, >= 1 */
+  int32_t dtype;            /* skv_dtype of Q, K, V, the output and both caches */
+  float softmax_scale;      /* logit scale; 0 selects 1/sqrt(head_dim) */
+  int64_t pos_offset;       /* virtual position of the first video token (room for a text prefix) */
+} skv_config;
+
+typedef struct skv_ctx skv_ctx;
+
+/* Validates cfg, allocates and zeroes every device buffer of one video stream
+ * (compressed state and decode cache of all layers, scratch), and binds the
+ * context to hip_stream (a hipStream_t; NULL means the default stream).
+ * Limits: pos_offset + max_frames * T < 2^31; B + T <= 16384.
+ * Returns SKV_OK and *out, or an error and *out = NULL. */
+skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
+
+/* Runs layers [layer_begin, layer_begin + layer_count) of the current frame n:
+ * attention with fused importance scoring (Eq. 5 and the score), Top-B refresh
+ * of each layer's compressed state (Eq. 6), and append of the frame's K/V to
+ * each layer's decode cache.  Layers of one frame must be stepped in order;
+ * the frame counter advances after the last layer.  layer_count = n_layers
+ * runs the whole stack in one launch per stage.
+ * Device layouts (row-major, dtype of the config):
+ *   q   [layer_count][H_q ][T][d]
+ *   k,v [layer_count][H_kv][T][d]
+ *   out [layer_count][H_q ][T][d]   attention output, written
+ * Errors: SKV_ERR_INVALID_ARG (null pointer, count out of range),
+ * SKV_ERR_ORDER, SKV_ERR_CAPACITY (n >= max_frames), SKV_ERR_DEVICE. */
+skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count,
+                          const void* q, const void* k, const void* v, void* out);
+
+/* Borrowed view of one layer's compressed state C (Eq. 4) and of the last
+ * step's candidate pool.  Slots are unordered; pos gives each slot's virtual
+ * position.  Pointers stay valid until skv_destroy; contents change with the
+ * next skv_frame_step.  The caller may write k, v, pos and score between steps
+ * (used to force a given state); the first `size` slots of every KV head are
+ * the state. */
+typedef struct {
+  void* k;                 /* [H_kv][capacity][d] */
+  void* v;                 /* [H_kv][capacity][d] */
+  int32_t* pos;            /* [H_kv][capacity] virtual positions */
+  float* score;            /* [H_kv][capacity] score at the frame that last selected the slot */
+  int32_t size;            /* valid slots per KV head = min(B, T * frames done by this layer) */
+  int32_t capacity;        /* B */
+  int64_t frame;           /* frames this layer has completed */
+  const float* pool_score; /* [H_kv][pool_stride] scores of the last step's candidates:
+                              state slots 0..size_before-1 first, then frame tokens 0..T-1 */
+  const int32_t* pool_pos; /* [H_kv][pool_stride] their virtual positions */
+  int32_t pool_size;       /* candidates in the last step (0 before the first) */
+  int32_t pool_stride;
+} skv_state_view_t;
+
+skv_status skv_state_view(skv_ctx* ctx, int32_t layer, skv_state_view_t* out);
+
+/* Borrowed view of one layer's decode cache D (Eq. 4): token rows in stream
+ * order, row r of KV head g at k + (g * max_tokens + r) * d.  Valid until
+ * skv_destroy. */
+typedef struct {
+  void* k;            /* [H_kv][max_tokens][d] */
+  void* v;            /* [H_kv][max_tokens][d] */
+  int64_t n_tokens;   /* rows written = T * frames done by this layer */
+  int64_t max_tokens; /* T * max_frames */
+  int32_t n_kv_heads;
+  int32_t head_dim;
+} skv_cache_view_t;
+
+skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* out);
+
+/* Starts a new video on the same context: frame counter and L_n return to 0,
+ * every state becomes empty.  Device contents are left as they are (nothing
+ * is enqueued). */
+skv_status skv_reset(skv_ctx* ctx);
+
+/* Sets the frame counter to `frame` (0 <= frame < max_frames) at layer 0, so
+ * that a caller can force a state through skv_state_view and run one step
+ * from it.  The state size becomes min(B, T * frame). */
+skv_status skv_seek(skv_ctx* ctx, int64_t frame);
+
+/* Kernel timing with HIP events on the context's stream.  skv_timing_start
+ * creates events for up to max_steps subsequent skv_frame_step calls (created
+ * here, never in the step).  skv_timing_stop synchronises the stream and
+ * writes ms[i * SKV_N_STAGES + s] for step i and stage s (attention, selection,
+ * state update, cache append), *n_steps the number of steps recorded, then
+ * releases the events. */
+enum { SKV_STAGE_ATTENTION = 0, SKV_STAGE_SELECT = 1, SKV_STAGE_UPDATE = 2, SKV_STAGE_APPEND = 3,
+       SKV_N_STAGES = 4 };
+skv_status skv_timing_start(skv_ctx* ctx, int32_t max_steps);
+skv_status skv_timing_stop(skv_ctx* ctx, int32_t* n_steps, float* ms, int32_t ms_capacity);
+
+/* Frees every device buffer of the context; NULL is a no-op.  The caller must
+ * make sure no enqueued work of the context is still running. */
+void skv_destroy(skv_ctx* ctx);
+
+/* Static, NUL-terminated name of a status. */
+const char* skv_status_string(skv_status s);
+
+/* Last error detail recorded on the calling thread (static storage). */
+const char* skv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STATEKV_H */

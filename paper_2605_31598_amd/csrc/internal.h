@@ -1,0 +1,78 @@
+// Internal launch interface of the StateKV frame-step kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace skv {
+
+// One attention launch covers `n_layers` consecutive layers of one frame.
+// Layer indices inside the struct are relative to the first layer of the call;
+// every pointer is already offset to that layer.
+struct AttnArgs {
+  const void* q;       // [n_layers][H_q][T][d]
+  const void* kf;      // [n_layers][H_kv][T][d]   frame keys
+  const void* vf;      // [n_layers][H_kv][T][d]   frame values
+  const void* ks;      // [n_layers][H_kv][B][d]   state keys (slots 0..S-1 valid)
+  const void* vs;      // [n_layers][H_kv][B][d]   state values
+  void* out;           // [n_layers][H_q][T][d]
+  float* partial;      // [n_layers][H_kv][n_qtiles][pool_stride] column sums of P per row tile
+  int n_layers, H_q, H_kv, G, T, B, S;
+  int n_qtiles, pool_stride;
+  float scale_log2;    // softmax scale * log2(e)
+};
+
+struct SelectArgs {
+  const float* partial;  // as in AttnArgs
+  int n_qtiles, pool_stride;
+  const int32_t* state_pos;  // [n_layers][H_kv][B]
+  float* state_score;        // [n_layers][H_kv][B]
+  float* pool_score;         // [n_layers][H_kv][pool_stride]
+  int32_t* pool_pos;         // [n_layers][H_kv][pool_stride]
+  int32_t* admit_src;        // [n_layers][H_kv][T]  frame token of the a-th admitted candidate
+  int32_t* admit_dst;        // [n_layers][H_kv][T]  state slot it goes to
+  int32_t* admit_count;      // [n_layers][H_kv]
+  int n_layers, H_kv, T, B, S;
+  int32_t frame_pos0;        // virtual position of frame token 0
+  float inv_T;
+};
+
+struct UpdateArgs {
+  const void* kf;            // [n_layers][H_kv][T][d]
+  const void* vf;
+  void* ks;                  // [n_layers][H_kv][B][d]
+  void* vs;
+  int32_t* state_pos;        // [n_layers][H_kv][B]
+  float* state_score;
+  const float* pool_score;   // [n_layers][H_kv][pool_stride]
+  const int32_t* admit_src;
+  const int32_t* admit_dst;
+  const int32_t* admit_count;
+  int n_layers, H_kv, T, B, S, pool_stride;
+  int row_bytes;             // d * element size, a multiple of 16
+  int32_t frame_pos0;
+};
+
+struct AppendArgs {
+  const void* kf;            // [n_layers][H_kv][T][d]
+  const void* vf;
+  void* ck;                  // [n_layers][H_kv][max_tokens][d]
+  void* cv;
+  int n_layers, H_kv, T;
+  int64_t max_tokens, first_row;  // first_row = frame * T
+  int row_bytes;
+};
+
+constexpr int kMfmaRowsPerTile = 256;   // query rows (G*T packed) per attention workgroup
+constexpr int kSimpleRowsPerTile = 64;
+constexpr int kSelectThreads = 1024;
+constexpr int kMaxPool = 16384;         // B + T limit (selection keeps the pool in LDS)
+
+hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
+hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride);
+
+}  // namespace skv

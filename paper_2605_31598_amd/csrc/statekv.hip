@@ -1,0 +1,435 @@
+// Host runtime of the StateKV frame step: configuration checks, one-time device
+// allocation, per-frame launch sequence and the C ABI of include/statekv.h.
+//
+// Per frame and layer range the stream receives, in order:
+//   1. attention + fused column sums of P     (Eq. 5 and the importance score)
+//   2. score finalisation + Top-B selection   (Eq. 6, ties to the lowest position)
+//   3. state update: admitted rows into evicted or free slots
+//   4. decode-cache append of the frame's K/V (Eq. 4, detailed state)
+// The state size S_n = min(B, n * T) and the frame's virtual positions
+// L_n + t are host-side bookkeeping (virtual sequence length paragraph), so the
+// step needs no device-to-host synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/statekv.h"
+#include "internal.h"
+
+namespace skv {
+hipError_t prepare_select(int pool_stride);
+hipError_t prepare_attention_mfma();
+}  // namespace skv
+
+namespace {
+
+thread_local std::string g_last_error;
+
+skv_status fail(skv_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+skv_status hip_fail(hipError_t e, const char* what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return SKV_ERR_DEVICE;
+}
+
+}  // namespace
+
+struct skv_ctx {
+  skv_config cfg{};
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int elem = 2;
+  int G = 1;
+  float scale_log2 = 0.f;
+  bool use_mfma = false;
+  int n_qtiles = 0;
+  int pool_stride = 0;
+  size_t row_bytes = 0;
+  int64_t max_tokens = 0;
+
+  // device buffers (one allocation each)
+  void* state_k = nullptr;   // [L][H_kv][B][d]
+  void* state_v = nullptr;
+  int32_t* state_pos = nullptr;    // [L][H_kv][B]
+  float* state_score = nullptr;
+  void* cache_k = nullptr;   // [L][H_kv][max_tokens][d]
+  void* cache_v = nullptr;
+  float* partial = nullptr;  // [L][H_kv][n_qtiles][pool_stride]
+  float* pool_score = nullptr;     // [L][H_kv][pool_stride]
+  int32_t* pool_pos = nullptr;
+  int32_t* admit_src = nullptr;    // [L][H_kv][T]
+  int32_t* admit_dst = nullptr;
+  int32_t* admit_count = nullptr;  // [L][H_kv]
+  std::vector<void*> allocations;
+
+  // progress of the stream
+  int64_t frame = 0;    // frame being processed
+  int next_layer = 0;   // next layer expected within that frame
+  std::vector<int32_t> last_pool;  // candidates of each layer's last step
+
+  // timing
+  std::vector<hipEvent_t> events;  // (SKV_N_STAGES + 1) per recorded step
+  int timing_max = 0, timing_n = 0;
+};
+
+namespace {
+
+skv_status alloc(skv_ctx* c, size_t bytes, void** out) {
+  void* p = nullptr;
+  const hipError_t e = hipMalloc(&p, bytes > 0 ? bytes : 16);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SKV_ERR_OUT_OF_MEMORY, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+  }
+  c->allocations.push_back(p);
+  *out = p;
+  return SKV_OK;
+}
+
+void release(skv_ctx* c) {
+  for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
+  c->events.clear();
+  for (void* p : c->allocations) (void)hipFree(p);
+  c->allocations.clear();
+}
+
+int layer_frames_done(const skv_ctx* c, int layer) {
+  return static_cast<int>(c->frame) + (layer < c->next_layer ? 1 : 0);
+}
+
+int state_size(const skv_ctx* c, int64_t frames_done) {
+  const int64_t seen = frames_done * c->cfg.tokens_per_frame;
+  return static_cast<int>(seen < c->cfg.capacity ? seen : c->cfg.capacity);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* skv_status_string(skv_status s) {
+  switch (s) {
+    case SKV_OK: return "SKV_OK";
+    case SKV_ERR_INVALID_ARG: return "SKV_ERR_INVALID_ARG";
+    case SKV_ERR_OUT_OF_MEMORY: return "SKV_ERR_OUT_OF_MEMORY";
+    case SKV_ERR_CAPACITY: return "SKV_ERR_CAPACITY";
+    case SKV_ERR_ORDER: return "SKV_ERR_ORDER";
+    case SKV_ERR_DEVICE: return "SKV_ERR_DEVICE";
+    case SKV_ERR_UNSUPPORTED: return "SKV_ERR_UNSUPPORTED";
+  }
+  return "SKV_STATUS_UNKNOWN";
+}
+
+const char* skv_last_error(void) { return g_last_error.c_str(); }
+
+skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
+  if (out == nullptr) return fail(SKV_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (cfg == nullptr) return fail(SKV_ERR_INVALID_ARG, "cfg is NULL");
+  const skv_config& c = *cfg;
+  if (c.n_layers < 1 || c.n_q_heads < 1 || c.n_kv_heads < 1 || c.tokens_per_frame < 1 || c.capacity < 0 ||
+      c.max_frames < 1)
+    return fail(SKV_ERR_INVALID_ARG, "sizes must be positive (capacity >= 0)");
+  if (c.n_q_heads % c.n_kv_heads != 0) return fail(SKV_ERR_INVALID_ARG, "n_q_heads must be a multiple of n_kv_heads");
+  if (c.head_dim != 64 && c.head_dim != 128) return fail(SKV_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c.dtype != SKV_BF16 && c.dtype != SKV_F32) return fail(SKV_ERR_INVALID_ARG, "unknown dtype");
+  if (!(c.softmax_scale >= 0.f) || !std::isfinite(c.softmax_scale))
+    return fail(SKV_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0");
+  if (c.pos_offset < 0) return fail(SKV_ERR_INVALID_ARG, "pos_offset must be >= 0");
+  const int64_t max_tokens = static_cast<int64_t>(c.max_frames) * c.tokens_per_frame;
+  if (c.pos_offset + max_tokens >= (int64_t{1} << 31)) return fail(SKV_ERR_INVALID_ARG, "positions exceed int32");
+  if (static_cast<int64_t>(c.capacity) + c.tokens_per_frame > skv::kMaxPool)
+    return fail(SKV_ERR_UNSUPPORTED, "capacity + tokens_per_frame exceeds 16384");
+  const int64_t rows = static_cast<int64_t>(c.n_q_heads / c.n_kv_heads) * c.tokens_per_frame;
+  if (rows >= (int64_t{1} << 30)) return fail(SKV_ERR_INVALID_ARG, "too many query rows per KV head");
+
+  skv_ctx* ctx = new skv_ctx();
+  ctx->cfg = c;
+  ctx->stream = static_cast<hipStream_t>(hip_stream);
+  ctx->elem = c.dtype == SKV_BF16 ? 2 : 4;
+  ctx->G = c.n_q_heads / c.n_kv_heads;
+  const float scale = c.softmax_scale > 0.f ? c.softmax_scale : 1.0f / std::sqrt(static_cast<float>(c.head_dim));
+  ctx->scale_log2 = scale * 1.4426950408889634f;
+  const char* force_simple = std::getenv("SKV_FORCE_SIMPLE_ATTENTION");
+  ctx->use_mfma = c.dtype == SKV_BF16 && !(force_simple && force_simple[0] == '1');
+  const int rows_per_tile = ctx->use_mfma ? skv::kMfmaRowsPerTile : skv::kSimpleRowsPerTile;
+  ctx->n_qtiles = static_cast<int>((rows + rows_per_tile - 1) / rows_per_tile);
+  ctx->pool_stride = ((c.capacity + c.tokens_per_frame + 63) / 64) * 64;
+  ctx->row_bytes = static_cast<size_t>(c.head_dim) * ctx->elem;
+  ctx->max_tokens = max_tokens;
+  ctx->last_pool.assign(c.n_layers, 0);
+
+  hipError_t e = hipGetDevice(&ctx->device);
+  if (e != hipSuccess) {
+    delete ctx;
+    return hip_fail(e, "hipGetDevice");
+  }
+  e = skv::prepare_kernels(c.head_dim, c.dtype == SKV_BF16, ctx->pool_stride);
+  if (e != hipSuccess) {
+    delete ctx;
+    return hip_fail(e, "kernel attributes");
+  }
+
+  const size_t LH = static_cast<size_t>(c.n_layers) * c.n_kv_heads;
+  const size_t state_bytes = LH * c.capacity * ctx->row_bytes;
+  const size_t cache_bytes = LH * static_cast<size_t>(max_tokens) * ctx->row_bytes;
+  struct Req { void** p; size_t bytes; };
+  const Req reqs[] = {
+      {&ctx->state_k, state_bytes},
+      {&ctx->state_v, state_bytes},
+      {reinterpret_cast<void**>(&ctx->state_pos), LH * c.capacity * sizeof(int32_t)},
+      {reinterpret_cast<void**>(&ctx->state_score), LH * c.capacity * sizeof(float)},
+      {&ctx->cache_k, cache_bytes},
+      {&ctx->cache_v, cache_bytes},
+      {reinterpret_cast<void**>(&ctx->partial), LH * ctx->n_qtiles * ctx->pool_stride * sizeof(float)},
+      {reinterpret_cast<void**>(&ctx->pool_score), LH * ctx->pool_stride * sizeof(float)},
+      {reinterpret_cast<void**>(&ctx->pool_pos), LH * ctx->pool_stride * sizeof(int32_t)},
+      {reinterpret_cast<void**>(&ctx->admit_src), LH * c.tokens_per_frame * sizeof(int32_t)},
+      {reinterpret_cast<void**>(&ctx->admit_dst), LH * c.tokens_per_frame * sizeof(int32_t)},
+      {reinterpret_cast<void**>(&ctx->admit_count), LH * sizeof(int32_t)},
+  };
+  for (const Req& r : reqs) {
+    const skv_status s = alloc(ctx, r.bytes, r.p);
+    if (s != SKV_OK) {
+      release(ctx);
+      delete ctx;
+      return s;
+    }
+    e = hipMemsetAsync(*r.p, 0, r.bytes > 0 ? r.bytes : 16, ctx->stream);
+    if (e != hipSuccess) {
+      release(ctx);
+      delete ctx;
+      return hip_fail(e, "hipMemsetAsync");
+    }
+  }
+  *out = ctx;
+  return SKV_OK;
+}
+
+skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, const void* q, const void* k,
+                          const void* v, void* out) {
+  if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr)
+    return fail(SKV_ERR_INVALID_ARG, "q, k, v and out must be device pointers");
+  const skv_config& c = ctx->cfg;
+  if (layer_count < 1 || layer_begin < 0 || layer_begin + layer_count > c.n_layers)
+    return fail(SKV_ERR_INVALID_ARG, "layer range outside [0, n_layers)");
+  if (layer_begin != ctx->next_layer)
+    return fail(SKV_ERR_ORDER, "expected layer_begin = " + std::to_string(ctx->next_layer));
+  if (ctx->frame >= c.max_frames) return fail(SKV_ERR_CAPACITY, "decode cache is full (max_frames reached)");
+
+  const int T = c.tokens_per_frame, Hkv = c.n_kv_heads, B = c.capacity, d = c.head_dim;
+  const int S = state_size(ctx, ctx->frame);
+  const int32_t pos0 = static_cast<int32_t>(c.pos_offset + ctx->frame * T);
+  const size_t lh0 = static_cast<size_t>(layer_begin) * Hkv;
+  const size_t rb = ctx->row_bytes;
+
+  const bool timing = ctx->timing_n < ctx->timing_max;
+  hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
+  auto mark = [&](int i) -> hipError_t { return timing ? hipEventRecord(ev[i], ctx->stream) : hipSuccess; };
+
+  skv::AttnArgs aa;
+  aa.q = q;
+  aa.kf = k;
+  aa.vf = v;
+  aa.ks = static_cast<char*>(ctx->state_k) + lh0 * B * rb;
+  aa.vs = static_cast<char*>(ctx->state_v) + lh0 * B * rb;
+  aa.out = out;
+  aa.partial = ctx->partial + lh0 * ctx->n_qtiles * ctx->pool_stride;
+  aa.n_layers = layer_count;
+  aa.H_q = c.n_q_heads;
+  aa.H_kv = Hkv;
+  aa.G = ctx->G;
+  aa.T = T;
+  aa.B = B;
+  aa.S = S;
+  aa.n_qtiles = ctx->n_qtiles;
+  aa.pool_stride = ctx->pool_stride;
+  aa.scale_log2 = ctx->scale_log2;
+
+  skv::SelectArgs sa;
+  sa.partial = aa.partial;
+  sa.n_qtiles = ctx->n_qtiles;
+  sa.pool_stride = ctx->pool_stride;
+  sa.state_pos = ctx->state_pos + lh0 * B;
+  sa.state_score = ctx->state_score + lh0 * B;
+  sa.pool_score = ctx->pool_score + lh0 * ctx->pool_stride;
+  sa.pool_pos = ctx->pool_pos + lh0 * ctx->pool_stride;
+  sa.admit_src = ctx->admit_src + lh0 * T;
+  sa.admit_dst = ctx->admit_dst + lh0 * T;
+  sa.admit_count = ctx->admit_count + lh0;
+  sa.n_layers = layer_count;
+  sa.H_kv = Hkv;
+  sa.T = T;
+  sa.B = B;
+  sa.S = S;
+  sa.frame_pos0 = pos0;
+  sa.inv_T = 1.0f / static_cast<float>(T);
+
+  skv::UpdateArgs ua;
+  ua.kf = k;
+  ua.vf = v;
+  ua.ks = const_cast<void*>(aa.ks);
+  ua.vs = const_cast<void*>(aa.vs);
+  ua.state_pos = ctx->state_pos + lh0 * B;
+  ua.state_score = sa.state_score;
+  ua.pool_score = sa.pool_score;
+  ua.admit_src = sa.admit_src;
+  ua.admit_dst = sa.admit_dst;
+  ua.admit_count = sa.admit_count;
+  ua.n_layers = layer_count;
+  ua.H_kv = Hkv;
+  ua.T = T;
+  ua.B = B;
+  ua.S = S;
+  ua.pool_stride = ctx->pool_stride;
+  ua.row_bytes = static_cast<int>(rb);
+  ua.frame_pos0 = pos0;
+
+  skv::AppendArgs pa;
+  pa.kf = k;
+  pa.vf = v;
+  pa.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
+  pa.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
+  pa.n_layers = layer_count;
+  pa.H_kv = Hkv;
+  pa.T = T;
+  pa.max_tokens = ctx->max_tokens;
+  pa.first_row = ctx->frame * T;
+  pa.row_bytes = static_cast<int>(rb);
+
+  hipError_t e = mark(0);
+  if (e == hipSuccess)
+    e = ctx->use_mfma ? skv::launch_attention_mfma_bf16(aa, d, ctx->stream)
+                      : skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream);
+  if (e == hipSuccess) e = mark(1);
+  if (e == hipSuccess) e = skv::launch_select(sa, ctx->stream);
+  if (e == hipSuccess) e = mark(2);
+  if (e == hipSuccess && B > 0) e = skv::launch_update(ua, ctx->stream);
+  if (e == hipSuccess) e = mark(3);
+  if (e == hipSuccess) e = skv::launch_append(pa, ctx->stream);
+  if (e == hipSuccess) e = mark(4);
+  if (e != hipSuccess) return hip_fail(e, "frame step launch");
+  if (timing) ++ctx->timing_n;
+
+  for (int l = layer_begin; l < layer_begin + layer_count; ++l) ctx->last_pool[l] = S + T;
+  ctx->next_layer += layer_count;
+  if (ctx->next_layer == c.n_layers) {
+    ctx->next_layer = 0;
+    ++ctx->frame;
+  }
+  return SKV_OK;
+}
+
+skv_status skv_state_view(skv_ctx* ctx, int32_t layer, skv_state_view_t* out) {
+  if (ctx == nullptr || out == nullptr) return fail(SKV_ERR_INVALID_ARG, "NULL argument");
+  const skv_config& c = ctx->cfg;
+  if (layer < 0 || layer >= c.n_layers) return fail(SKV_ERR_INVALID_ARG, "layer out of range");
+  const size_t lh = static_cast<size_t>(layer) * c.n_kv_heads;
+  const int done = layer_frames_done(ctx, layer);
+  out->k = static_cast<char*>(ctx->state_k) + lh * c.capacity * ctx->row_bytes;
+  out->v = static_cast<char*>(ctx->state_v) + lh * c.capacity * ctx->row_bytes;
+  out->pos = ctx->state_pos + lh * c.capacity;
+  out->score = ctx->state_score + lh * c.capacity;
+  out->size = state_size(ctx, done);
+  out->capacity = c.capacity;
+  out->frame = done;
+  out->pool_score = ctx->pool_score + lh * ctx->pool_stride;
+  out->pool_pos = ctx->pool_pos + lh * ctx->pool_stride;
+  out->pool_size = ctx->last_pool[layer];
+  out->pool_stride = ctx->pool_stride;
+  return SKV_OK;
+}
+
+skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* out) {
+  if (ctx == nullptr || out == nullptr) return fail(SKV_ERR_INVALID_ARG, "NULL argument");
+  const skv_config& c = ctx->cfg;
+  if (layer < 0 || layer >= c.n_layers) return fail(SKV_ERR_INVALID_ARG, "layer out of range");
+  const size_t lh = static_cast<size_t>(layer) * c.n_kv_heads;
+  out->k = static_cast<char*>(ctx->cache_k) + lh * ctx->max_tokens * ctx->row_bytes;
+  out->v = static_cast<char*>(ctx->cache_v) + lh * ctx->max_tokens * ctx->row_bytes;
+  out->n_tokens = static_cast<int64_t>(layer_frames_done(ctx, layer)) * c.tokens_per_frame;
+  out->max_tokens = ctx->max_tokens;
+  out->n_kv_heads = c.n_kv_heads;
+  out->head_dim = c.head_dim;
+  return SKV_OK;
+}
+
+skv_status skv_reset(skv_ctx* ctx) {
+  if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
+  ctx->frame = 0;
+  ctx->next_layer = 0;
+  std::fill(ctx->last_pool.begin(), ctx->last_pool.end(), 0);
+  return SKV_OK;
+}
+
+skv_status skv_seek(skv_ctx* ctx, int64_t frame) {
+  if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
+  if (frame < 0 || frame >= ctx->cfg.max_frames) return fail(SKV_ERR_INVALID_ARG, "frame out of range");
+  ctx->frame = frame;
+  ctx->next_layer = 0;
+  return SKV_OK;
+}
+
+skv_status skv_timing_start(skv_ctx* ctx, int32_t max_steps) {
+  if (ctx == nullptr || max_steps < 1) return fail(SKV_ERR_INVALID_ARG, "bad timing request");
+  for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
+  ctx->events.assign(static_cast<size_t>(max_steps) * (SKV_N_STAGES + 1), nullptr);
+  for (auto& e : ctx->events) {
+    const hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      ctx->timing_max = 0;
+      return hip_fail(r, "hipEventCreate");
+    }
+  }
+  ctx->timing_max = max_steps;
+  ctx->timing_n = 0;
+  return SKV_OK;
+}
+
+skv_status skv_timing_stop(skv_ctx* ctx, int32_t* n_steps, float* ms, int32_t ms_capacity) {
+  if (ctx == nullptr || n_steps == nullptr || ms == nullptr) return fail(SKV_ERR_INVALID_ARG, "NULL argument");
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  const int n = ctx->timing_n < ms_capacity / SKV_N_STAGES ? ctx->timing_n : ms_capacity / SKV_N_STAGES;
+  for (int i = 0; i < n; ++i) {
+    hipEvent_t* ev = &ctx->events[static_cast<size_t>(i) * (SKV_N_STAGES + 1)];
+    for (int s = 0; s < SKV_N_STAGES; ++s) {
+      float t = 0.f;
+      e = hipEventElapsedTime(&t, ev[s], ev[s + 1]);
+      if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+      ms[i * SKV_N_STAGES + s] = t;
+    }
+  }
+  *n_steps = n;
+  for (hipEvent_t ev : ctx->events) (void)hipEventDestroy(ev);
+  ctx->events.clear();
+  ctx->timing_max = ctx->timing_n = 0;
+  return SKV_OK;
+}
+
+void skv_destroy(skv_ctx* ctx) {
+  if (ctx == nullptr) return;
+  release(ctx);
+  delete ctx;
+}
+
+}  // extern "C"
+
+namespace skv {
+
+hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride) {
+  (void)head_dim;
+  hipError_t e = prepare_select(pool_stride);
+  if (e != hipSuccess) return e;
+  if (bf16) e = prepare_attention_mfma();
+  return e;
+}
+
+}  // namespace skv
