@@ -13,10 +13,10 @@
 //   * Keys stream through LDS in tiles of 64, double buffered; K row-major,
 //     V transposed (V^T) so both MFMA operands are 16-byte LDS reads.
 //   * Two sweeps over the keys.  Sweep 1: S^T = K Q^T -> per-row max and sum of
-//     exp2 -> lse2.  Sweep 2: S^T again -> exact P^T = exp2(x - lse2) ->
-//     O^T += V^T P^T and per-key column sums of P.  Exact probabilities are known
-//     only after the row statistics, and recomputing K Q^T is cheaper than
-//     storing the logits.
+//     exp2.  Sweep 2: S^T again -> E^T = exp2(x - row max) -> O^T += V^T E^T
+//     (scaled by 1/sum at the end) and per-key column sums of P = E / sum.
+//     Exact probabilities are known only after the row statistics, and
+//     recomputing K Q^T is cheaper than storing the logits.
 //   * The blockIdx -> tile mapping keeps the row tiles of one (layer, KV head)
 //     on one XCD so they share K/V in that XCD's L2.
 //
@@ -266,7 +266,9 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
           float sum = 0.f;
 #pragma unroll
           for (int v = 0; v < 16; ++v) sum += fast_exp2(fmaf(z[v], c, -mc));
-          l[qb] = l[qb] * fast_exp2(fmaf(m[qb], c, -mc)) + sum;
+          // Subtract before scaling: equal maxima (including the empty-row sentinel)
+          // give exactly exp2(0) = 1.
+          l[qb] = l[qb] * fast_exp2((m[qb] - mn) * c) + sum;
           m[qb] = mn;
         }
       }
@@ -274,7 +276,10 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
     if (more) store_k(b ^ 1);
     __syncthreads();
   }
-  float lse2[kQB];
+  // Row maximum (log2 units) and 1/sum.  Sweep 2 feeds the PV MFMA with
+  // E = exp2(x - max) <= 1, whose largest entry is exactly 1 in bf16, and applies
+  // 1/sum in fp32 to the output; the column sums use P = E / sum in fp32.
+  float mrow[kQB], inv_l[kQB];
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) {
     // the other 16 keys of every 32-key block live in lane ^ 32
@@ -282,7 +287,9 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
     const float lo = __shfl_xor(l[qb], 32, 64);
     const float mm = fmaxf(m[qb], mo);
     const float ll = l[qb] * fast_exp2((m[qb] - mm) * c) + lo * fast_exp2((mo - mm) * c);
-    lse2[qb] = lim[qb] >= 0 ? mm * c + fast_log2(ll) : __builtin_huge_valf();
+    const bool valid = lim[qb] >= 0;
+    mrow[qb] = valid ? mm * c : 0.f;
+    inv_l[qb] = valid ? 1.0f / ll : 0.f;
   }
 
   // ---------------- sweep 2: P, O and column sums ----------------
@@ -314,20 +321,20 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
         f32x16 acc[kQB];
         qk_block(b, kb, acc);
         const int jb = t * kKT + kb * 32 + 4 * h;
-        float p[kQB][16];
+        float p[kQB][16];  // E = exp2(x - row max), masked entries 0
 #pragma unroll
         for (int qb = 0; qb < kQB; ++qb) {
           const int rel = lim[qb] - jb;
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            float x = fast_exp2(fmaf(acc[qb][v], c, -lse2[qb]));
+            float x = fast_exp2(fmaf(acc[qb][v], c, -mrow[qb]));
             if (masked && 8 * (v >> 2) + (v & 3) > rel) x = 0.f;
             p[qb][v] = x;
           }
         }
-        float cs[16];
+        float cs[16];  // P = E / sum, added over the lane's two rows
 #pragma unroll
-        for (int v = 0; v < 16; ++v) cs[v] = p[0][v] + p[1][v];
+        for (int v = 0; v < 16; ++v) cs[v] = fmaf(p[0][v], inv_l[0], p[1][v] * inv_l[1]);
         bf16x8 pb[kQB][2];
 #pragma unroll
         for (int qb = 0; qb < kQB; ++qb)
@@ -377,7 +384,7 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
         for (int vq = 0; vq < 4; ++vq) {
           __bf16 w[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) w[u] = static_cast<__bf16>(o[qb][db][vq * 4 + u]);
+          for (int u = 0; u < 4; ++u) w[u] = static_cast<__bf16>(o[qb][db][vq * 4 + u] * inv_l[qb]);
           uint2 packed;
           packed.x = static_cast<unsigned>(__builtin_bit_cast(uint16_t, w[0])) |
                      (static_cast<unsigned>(__builtin_bit_cast(uint16_t, w[1])) << 16);

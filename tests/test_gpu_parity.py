@@ -177,7 +177,7 @@ def test_device_generator_matches_host():
     got = out.view(torch.int16).cpu().numpy().view(np.uint16)
     for i, (l, f) in enumerate([(0, 0), (3, 17), (27, 511)]):
         assert np.array_equal(got[i], gen.frame_inputs(wl, l, f)["q"].reshape(-1))
-    out32 = torch.empty((1, 4 * 16 * 64), dtype=torch.float32, device="cuda")
+    out32 = torch.empty((1, 2 * 16 * 64), dtype=torch.float32, device="cuda")  # V is [H_kv=2][T=16][d=64]
     t = CONFIGS["tiny_f32"]
     device.fill_iid(out32, [gen.stream_key(t.seed, 0, 5, gen.TENSOR_V)], "f32")
     assert np.array_equal(out32.cpu().numpy()[0], gen.frame_inputs(t, 0, 5)["v"].reshape(-1))
