@@ -138,6 +138,8 @@ def main():
     ap.add_argument("--workload", default="vlm7b_28layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the step shards by KV head "
@@ -150,6 +152,16 @@ def main():
     from workloads import CONFIGS
     from workloads import device as wdev
     from workloads import generate as gen
+
+    if args.copy_calibration:
+        src = torch.ones(1 << 29, dtype=torch.int16, device="cuda")  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": src.numel() * 2, "copy_calibration_bytes_written": src.numel() * 2,
+                          "launches": 3}))
+        return
 
     wl = CONFIGS[args.workload]
     if wl.dtype != "bf16":

@@ -7,58 +7,67 @@
 // divides by T (the importance score of the attention-driven selection).
 //
 // Work decomposition
-//   * A workgroup owns 256 query rows of one (layer, KV head).  Rows are the G
-//     query heads sharing the KV head times the T frame tokens (grouped-query
-//     packing: every row of the tile reads the same K/V).  4 waves x 64 rows.
-//   * Keys stream through LDS in tiles of 64, double buffered; K row-major,
-//     V transposed (V^T) so both MFMA operands are 16-byte LDS reads.
+//   * A workgroup owns 256 query rows of one (layer, KV head): 8 waves x 32 rows,
+//     two waves per SIMD.  Rows are the G query heads sharing the KV head times
+//     the T frame tokens (grouped-query packing: every row of the tile reads the
+//     same K/V).  Two waves per SIMD let the hardware run one wave's exp/softmax
+//     VALU work under the other wave's MFMAs; a single wave does not overlap its
+//     own MFMA and VALU streams well on gfx950.
+//   * Keys stream through LDS in tiles of 64 (two 32-key blocks), double
+//     buffered, K and V both row-major; the next tile's global loads are issued
+//     before the current tile's compute.
 //   * Two sweeps over the keys.  Sweep 1: S^T = K Q^T -> per-row max and sum of
-//     exp2.  Sweep 2: S^T again -> E^T = exp2(x - row max) -> O^T += V^T E^T
-//     (scaled by 1/sum at the end) and per-key column sums of P = E / sum.
-//     Exact probabilities are known only after the row statistics, and
-//     recomputing K Q^T is cheaper than storing the logits.
+//     exp2.  Sweep 2: S^T again -> E = exp2(x - row max) -> O += E V (scaled by
+//     1/sum at the end) and per-key column sums of P = E / sum.  Exact
+//     probabilities are known only after the row statistics, and recomputing
+//     K Q^T is cheaper than storing the logits.
+//   * Tiles that contain frame keys (the only ones with masked entries) run in a
+//     separate loop, keeping mask code off the common path.
 //   * The blockIdx -> tile mapping keeps the row tiles of one (layer, KV head)
 //     on one XCD so they share K/V in that XCD's L2.
 //
 // MFMA v_mfma_f32_32x32x16_bf16 (wave64) operand layout, lane l, h = l / 32:
 //   A (32x16): A[l % 32][8h .. 8h+7]   B (16x32): B[8h .. 8h+7][l % 32]
 //   C (32x32): element v (0..15) of lane l is C[8(v/4) + 4h + v%4][l % 32].
-// With S^T = K Q^T (M = keys, N = query rows, K = head dim) the C registers of
-// one lane hold 16 keys of one query row, so P^T can feed the B operand of
-// O^T = V^T P^T directly: the 8 values v = 8s..8s+7 of lane l are keys
-// 16s + {0..3, 8..11} (h = 0) or 16s + {4..7, 12..15} (h = 1).  V^T is stored
-// in LDS with bits 2 and 3 of the key index swapped inside each 16-key group,
-// which puts exactly those keys at consecutive addresses.
+// With S^T = K Q^T (M = keys, N = query rows, K = head dim) lane l holds 16
+// keys of query row l % 32, which is the A-operand shape of O = P V once the
+// contraction index k = 8h + i of k-step s is taken to mean key
+// 16s + 4h + (i < 4 ? i : i + 4).  The matching B operand (V rows of those keys,
+// one column per lane) comes from ds_read_b64_tr_b16: inside each group of 16
+// lanes, lane j points at V[k0 + j/4][d0 + 4(j%4)] and receives
+// V[k0 .. k0+3][d0 + j].
 #include "internal.h"
+
+#include <type_traits>
 
 namespace skv {
 
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kWaves = 4;
-constexpr int kQB = 2;         // 32-row blocks per wave
-constexpr int kRowsWave = 64;  // kQB * 32
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
+constexpr int kRowsWave = 32;
 constexpr int kKT = 64;        // keys per LDS tile (two 32-key blocks)
-constexpr int kPad = 8;        // bf16 padding per LDS row (16 bytes)
+constexpr int kPadK = 8;       // K row padding (bf16): 16-byte reads conflict-free
+constexpr int kPadV = 16;      // V row padding (bf16): transpose reads conflict-free
+constexpr int kPadO = 8;       // output staging row padding (bf16)
 static_assert(kWaves * kRowsWave == kMfmaRowsPerTile, "tile rows");
 
 template <int D>
 struct Smem {
-  uint16_t k[2][kKT][D + kPad];     // K rows
-  uint16_t vt[2][D][kKT + kPad];    // V^T, key order permuted inside 16-key groups
-  float cs[2][kWaves][kKT];         // per-wave column sums of the current tile
+  uint16_t k[2][kKT][D + kPadK];
+  uint16_t v[2][kKT][D + kPadV];
+  float cs[2][kWaves][kKT];     // per-wave column sums of one tile
+  float il[kWaves][kRowsWave];  // 1 / row sum, for the output
 };
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }  // v_exp_f32
-__device__ inline float fast_log2(float x) { return __builtin_amdgcn_logf(x); }   // v_log_f32
-
-__device__ inline int vt_slot(int kk) {  // swap bits 2 and 3 of the key index
-  return (kk & ~12) | ((kk & 4) << 1) | ((kk & 8) >> 1);
-}
 
 template <int CTRL>
 __device__ inline float dpp_f(float x) {
@@ -104,13 +113,12 @@ __device__ inline float column_reduce(const float (&cs)[16], int lane) {
 }  // namespace
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
-  constexpr int KS = D / 16;                       // k-steps of K Q^T
-  constexpr int DB = D / 32;                       // 32-row blocks of O^T
-  constexpr int KCH = D / 8;                       // 16-byte chunks per K/V row
-  constexpr int K_ITEMS = kKT * KCH / 256;         // K chunks staged per thread
-  constexpr int V_ITEMS = (kKT / 2) * KCH / 256;   // (key pair, chunk) units per thread
-  static_assert(K_ITEMS * 256 == kKT * KCH && V_ITEMS * 256 == (kKT / 2) * KCH, "staging split");
+__global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
+  constexpr int KS = D / 16;                   // k-steps of K Q^T
+  constexpr int DB = D / 32;                   // 32-column blocks of O
+  constexpr int KCH = D / 8;                   // 16-byte chunks per K/V row
+  constexpr int ITEMS = kKT * KCH / kThreads;  // chunks of one tile staged per thread
+  static_assert(ITEMS * kThreads == kKT * KCH, "staging split");
 
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   Smem<D>& sm = *reinterpret_cast<Smem<D>*>(smem_raw);
@@ -131,8 +139,9 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
   const int GT = a.G * a.T;
   const int S = a.S, n_keys = a.S + a.T;
   const int n_tiles = (n_keys + kKT - 1) / kKT;
+  const int first_masked = S / kKT;  // tiles from here on contain frame keys or the ragged end
   const int row0 = qt * kMfmaRowsPerTile + wave * kRowsWave;
-  const bool wave_active = row0 < GT;
+  const bool active = row0 < GT;
   const float c = a.scale_log2;
 
   const uint16_t* qg = static_cast<const uint16_t*>(a.q) + static_cast<size_t>(layer * a.H_q + g * a.G) * a.T * D;
@@ -140,217 +149,154 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
   const uint16_t* vst = static_cast<const uint16_t*>(a.vs) + static_cast<size_t>(lg) * a.B * D;
   const uint16_t* kfr = static_cast<const uint16_t*>(a.kf) + static_cast<size_t>(lg) * a.T * D;
   const uint16_t* vfr = static_cast<const uint16_t*>(a.vf) + static_cast<size_t>(lg) * a.T * D;
+  float* part = a.partial + (static_cast<size_t>(lg) * a.n_qtiles + qt) * a.pool_stride;
 
-  // Q^T operand (B of K Q^T) in registers; invalid rows are zero.
-  bf16x8 qreg[kQB][KS];
-  int lim[kQB];  // candidate j is visible to the row iff j <= lim (state keys, then causal frame)
+  // Q^T operand (B of K Q^T) in registers; an invalid row is zero and sees no key.
+  const int r_lane = row0 + l32;
+  const bool row_valid = r_lane < GT;
+  const int lim = row_valid ? S + (r_lane % a.T) : -1;  // candidate j is visible iff j <= lim
+  bf16x8 qreg[KS];
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const int r = row0 + qb * 32 + l32;
-    const bool valid = r < GT;
-    lim[qb] = valid ? S + (r % a.T) : -1;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      u32x4 x = {0u, 0u, 0u, 0u};
-      if (valid) x = *reinterpret_cast<const u32x4*>(qg + static_cast<size_t>(r) * D + ks * 16 + h * 8);
-      qreg[qb][ks] = __builtin_bit_cast(bf16x8, x);
-    }
+  for (int ks = 0; ks < KS; ++ks) {
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (row_valid) x = *reinterpret_cast<const u32x4*>(qg + static_cast<size_t>(r_lane) * D + ks * 16 + h * 8);
+    qreg[ks] = __builtin_bit_cast(bf16x8, x);
   }
 
-  auto row_ptr = [&](const uint16_t* st, const uint16_t* fr, int j) -> const uint16_t* {
-    return j < S ? st + static_cast<size_t>(j) * D : fr + static_cast<size_t>(j - S) * D;
-  };
-
-  u32x4 kpre[K_ITEMS];
-  u32x4 vpre[V_ITEMS][2];
-  auto load_k = [&](int t) {
+  // ---------------- staging (global -> registers -> LDS) ----------------
+  u32x4 kpre[ITEMS], vpre[ITEMS];
+  auto load_tile = [&](int t, bool with_v) {
 #pragma unroll
-    for (int it = 0; it < K_ITEMS; ++it) {
-      const int idx = it * 256 + tid;
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = it * kThreads + tid;
       const int kk = idx / KCH, ch = idx % KCH;
       const int j = t * kKT + kk;
-      u32x4 x = {0u, 0u, 0u, 0u};
-      if (j < n_keys) x = *reinterpret_cast<const u32x4*>(row_ptr(kst, kfr, j) + ch * 8);
+      u32x4 x = {0u, 0u, 0u, 0u}, y = {0u, 0u, 0u, 0u};
+      if (j < S) {
+        x = *reinterpret_cast<const u32x4*>(kst + static_cast<size_t>(j) * D + ch * 8);
+        if (with_v) y = *reinterpret_cast<const u32x4*>(vst + static_cast<size_t>(j) * D + ch * 8);
+      } else if (j < n_keys) {
+        x = *reinterpret_cast<const u32x4*>(kfr + static_cast<size_t>(j - S) * D + ch * 8);
+        if (with_v) y = *reinterpret_cast<const u32x4*>(vfr + static_cast<size_t>(j - S) * D + ch * 8);
+      }
       kpre[it] = x;
+      vpre[it] = y;
     }
   };
-  auto store_k = [&](int b) {
+  auto store_tile = [&](int b, bool with_v) {
 #pragma unroll
-    for (int it = 0; it < K_ITEMS; ++it) {
-      const int idx = it * 256 + tid;
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = it * kThreads + tid;
       const int kk = idx / KCH, ch = idx % KCH;
       *reinterpret_cast<u32x4*>(&sm.k[b][kk][ch * 8]) = kpre[it];
-    }
-  };
-  auto load_v = [&](int t) {
-#pragma unroll
-    for (int it = 0; it < V_ITEMS; ++it) {
-      const int idx = it * 256 + tid;
-      const int p = idx % (kKT / 2), ch = idx / (kKT / 2);
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int j = t * kKT + 2 * p + e;
-        u32x4 x = {0u, 0u, 0u, 0u};
-        if (j < n_keys) x = *reinterpret_cast<const u32x4*>(row_ptr(vst, vfr, j) + ch * 8);
-        vpre[it][e] = x;
-      }
-    }
-  };
-  auto store_v = [&](int b) {
-#pragma unroll
-    for (int it = 0; it < V_ITEMS; ++it) {
-      const int idx = it * 256 + tid;
-      const int p = idx % (kKT / 2), ch = idx / (kKT / 2);
-      const int col = vt_slot(2 * p);  // even; key 2p+1 lands at col + 1
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const unsigned x0 = vpre[it][0][w], x1 = vpre[it][1][w];
-        // element 2w and 2w+1 of the chunk: pair (key 2p, key 2p+1) per d
-        const unsigned lo = (x0 & 0xFFFFu) | (x1 << 16);
-        const unsigned hi = (x0 >> 16) | (x1 & 0xFFFF0000u);
-        *reinterpret_cast<unsigned*>(&sm.vt[b][ch * 8 + 2 * w][col]) = lo;
-        *reinterpret_cast<unsigned*>(&sm.vt[b][ch * 8 + 2 * w + 1][col]) = hi;
-      }
+      if (with_v) *reinterpret_cast<u32x4*>(&sm.v[b][kk][ch * 8]) = vpre[it];
     }
   };
 
-  // S^T block (32 keys x 32 rows) for key block kb of the tile in buffer b.
-  auto qk_block = [&](int b, int kb, f32x16 (&acc)[kQB]) {
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) acc[qb] = f32x16{};
+  // S^T block (32 keys x 32 rows) for key block kb of buffer b.
+  auto qk = [&](int b, int kb) -> f32x16 {
+    f32x16 acc = {};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const u32x4 x = *reinterpret_cast<const u32x4*>(&sm.k[b][kb * 32 + l32][ks * 16 + h * 8]);
-      const bf16x8 av = __builtin_bit_cast(bf16x8, x);
-#pragma unroll
-      for (int qb = 0; qb < kQB; ++qb)
-        acc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[qb][ks], acc[qb], 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, x), qreg[ks], acc, 0, 0, 0);
     }
+    return acc;
   };
 
-  // ---------------- sweep 1: row statistics ----------------
-  float m[kQB], l[kQB];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) { m[qb] = -1e30f; l[qb] = 0.f; }
-
-  load_k(0);
-  store_k(0);
-  __syncthreads();
-  for (int t = 0; t < n_tiles; ++t) {
+  // ============================ sweep 1: row statistics ============================
+  float m = -1e30f, l = 0.f;
+  auto sweep1_tile = [&](int t, auto masked) {
     const int b = t & 1;
-    const bool more = t + 1 < n_tiles;
-    if (more) load_k(t + 1);
-    if (wave_active) {
-      const bool masked = t * kKT + kKT > S;
+    if (t + 1 < n_tiles) load_tile(t + 1, false);
+    if (active) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        f32x16 acc[kQB];
-        qk_block(b, kb, acc);
-        const int jb = t * kKT + kb * 32 + 4 * h;
+        const f32x16 acc = qk(b, kb);
+        float z[16];
 #pragma unroll
-        for (int qb = 0; qb < kQB; ++qb) {
-          float z[16];
+        for (int v = 0; v < 16; ++v) z[v] = acc[v];
+        if constexpr (decltype(masked)::value) {
+          const int rel = lim - (t * kKT + kb * 32 + 4 * h);
 #pragma unroll
-          for (int v = 0; v < 16; ++v) z[v] = acc[qb][v];
-          if (masked) {
-            const int rel = lim[qb] - jb;
-#pragma unroll
-            for (int v = 0; v < 16; ++v)
-              if (8 * (v >> 2) + (v & 3) > rel) z[v] = -__builtin_huge_valf();
-          }
-          float mx = z[0];
-#pragma unroll
-          for (int v = 1; v < 16; ++v) mx = fmaxf(mx, z[v]);
-          const float mn = fmaxf(m[qb], mx);
-          const float mc = mn * c;
-          float sum = 0.f;
-#pragma unroll
-          for (int v = 0; v < 16; ++v) sum += fast_exp2(fmaf(z[v], c, -mc));
-          // Subtract before scaling: equal maxima (including the empty-row sentinel)
-          // give exactly exp2(0) = 1.
-          l[qb] = l[qb] * fast_exp2((m[qb] - mn) * c) + sum;
-          m[qb] = mn;
+          for (int v = 0; v < 16; ++v)
+            if (8 * (v >> 2) + (v & 3) > rel) z[v] = -__builtin_huge_valf();
         }
+        float mx = z[0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) mx = fmaxf(mx, z[v]);
+        const float mn = fmaxf(m, mx);
+        const float mc = mn * c;
+        float sum = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sum += fast_exp2(fmaf(z[v], c, -mc));
+        // Subtract before scaling: equal maxima (including the empty-row sentinel)
+        // give exactly exp2(0) = 1.
+        l = l * fast_exp2((m - mn) * c) + sum;
+        m = mn;
       }
     }
-    if (more) store_k(b ^ 1);
+    if (t + 1 < n_tiles) store_tile(b ^ 1, false);
     __syncthreads();
-  }
+  };
+  load_tile(0, false);
+  store_tile(0, false);
+  __syncthreads();
+  for (int t = 0; t < first_masked && t < n_tiles; ++t) sweep1_tile(t, std::false_type{});
+  for (int t = first_masked; t < n_tiles; ++t) sweep1_tile(t, std::true_type{});
+
   // Row maximum (log2 units) and 1/sum.  Sweep 2 feeds the PV MFMA with
   // E = exp2(x - max) <= 1, whose largest entry is exactly 1 in bf16, and applies
-  // 1/sum in fp32 to the output; the column sums use P = E / sum in fp32.
-  float mrow[kQB], inv_l[kQB];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
+  // 1/sum in fp32 to the output; the column sums use P = E / sum.
+  float mrow, inv_l;
+  {
     // the other 16 keys of every 32-key block live in lane ^ 32
-    const float mo = __shfl_xor(m[qb], 32, 64);
-    const float lo = __shfl_xor(l[qb], 32, 64);
-    const float mm = fmaxf(m[qb], mo);
-    const float ll = l[qb] * fast_exp2((m[qb] - mm) * c) + lo * fast_exp2((mo - mm) * c);
-    const bool valid = lim[qb] >= 0;
-    mrow[qb] = valid ? mm * c : 0.f;
-    inv_l[qb] = valid ? 1.0f / ll : 0.f;
+    const float mo = __shfl_xor(m, 32, 64);
+    const float lo = __shfl_xor(l, 32, 64);
+    const float mm = fmaxf(m, mo);
+    const float ll = l * fast_exp2((m - mm) * c) + lo * fast_exp2((mo - mm) * c);
+    mrow = row_valid ? mm * c : 0.f;
+    inv_l = row_valid ? 1.0f / ll : 0.f;
   }
 
-  // ---------------- sweep 2: P, O and column sums ----------------
-  f32x16 o[kQB][DB];
+  // ======================== sweep 2: P, O and column sums ========================
+  f32x16 o[DB];
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[qb][db] = f32x16{};
+  for (int db = 0; db < DB; ++db) o[db] = f32x16{};
 
-  float* part = a.partial + (static_cast<size_t>(lg) * a.n_qtiles + qt) * a.pool_stride;
   const int key_lane = 8 * (((lane >> 3) & 1) + 2 * ((lane >> 4) & 1)) + 4 * h + (((lane >> 1) & 1) + 2 * ((lane >> 2) & 1));
+  // transpose-read coordinates of this lane inside its 16-lane group
+  const int tr_row = 4 * h + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  load_k(0);
-  load_v(0);
-  store_k(0);
-  store_v(0);
-  __syncthreads();
-  for (int t = 0; t < n_tiles; ++t) {
+  auto sweep2_tile = [&](int t, auto masked) {
     const int b = t & 1;
-    const bool more = t + 1 < n_tiles;
-    if (more) {
-      load_k(t + 1);
-      load_v(t + 1);
-    }
-    if (wave_active) {
-      const bool masked = t * kKT + kKT > S;
+    if (t + 1 < n_tiles) load_tile(t + 1, true);
+    if (active) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        f32x16 acc[kQB];
-        qk_block(b, kb, acc);
-        const int jb = t * kKT + kb * 32 + 4 * h;
-        float p[kQB][16];  // E = exp2(x - row max), masked entries 0
+        const f32x16 acc = qk(b, kb);
+        const int rel = lim - (t * kKT + kb * 32 + 4 * h);
+        bf16x8 pe[2];
+        float cs[16];
 #pragma unroll
-        for (int qb = 0; qb < kQB; ++qb) {
-          const int rel = lim[qb] - jb;
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float x = fast_exp2(fmaf(acc[qb][v], c, -mrow[qb]));
-            if (masked && 8 * (v >> 2) + (v & 3) > rel) x = 0.f;
-            p[qb][v] = x;
+        for (int v = 0; v < 16; ++v) {
+          float e = fast_exp2(fmaf(acc[v], c, -mrow));
+          if constexpr (decltype(masked)::value) {
+            if (8 * (v >> 2) + (v & 3) > rel) e = 0.f;
           }
+          pe[v >> 3][v & 7] = static_cast<__bf16>(e);
+          cs[v] = e * inv_l;
         }
-        float cs[16];  // P = E / sum, added over the lane's two rows
 #pragma unroll
-        for (int v = 0; v < 16; ++v) cs[v] = fmaf(p[0][v], inv_l[0], p[1][v] * inv_l[1]);
-        bf16x8 pb[kQB][2];
+        for (int s = 0; s < 2; ++s) {
+          const int r = kb * 32 + s * 16 + tr_row;
 #pragma unroll
-        for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-          for (int s = 0; s < 2; ++s)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) pb[qb][s][i] = static_cast<__bf16>(p[qb][8 * s + i]);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-#pragma unroll
-          for (int s = 0; s < 2; ++s) {
-            const u32x4 x = *reinterpret_cast<const u32x4*>(&sm.vt[b][db * 32 + l32][kb * 32 + s * 16 + h * 8]);
-            const bf16x8 av = __builtin_bit_cast(bf16x8, x);
-#pragma unroll
-            for (int qb = 0; qb < kQB; ++qb)
-              o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[qb][s], o[qb][db], 0, 0, 0);
+          for (int db = 0; db < DB; ++db) {
+            const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(&sm.v[b][r][db * 32 + tr_col]));
+            const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(&sm.v[b][r + 8][db * 32 + tr_col]));
+            const bf16x8 vb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pe[s], vb, o[db], 0, 0, 0);
           }
         }
         const float tot = column_reduce(cs, lane);
@@ -359,40 +305,50 @@ __global__ __launch_bounds__(256, 1) void attn_mfma_kernel(AttnArgs a) {
     } else {
       sm.cs[b][wave][lane] = 0.f;
     }
-    if (more) {
-      store_k(b ^ 1);
-      store_v(b ^ 1);
-    }
+    if (t + 1 < n_tiles) store_tile(b ^ 1, true);
     __syncthreads();
+    // cross-wave column sums of tile t -> this row tile's partials; buffer b is
+    // written again only after the next barrier
     if (tid < kKT) {
       const int j = t * kKT + tid;
-      if (j < n_keys) part[j] = (sm.cs[b][0][tid] + sm.cs[b][1][tid]) + (sm.cs[b][2][tid] + sm.cs[b][3][tid]);
+      if (j < n_keys) {
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) sum += sm.cs[b][w][tid];
+        part[j] = sum;
+      }
+    }
+  };
+  load_tile(0, true);
+  store_tile(0, true);
+  __syncthreads();
+  for (int t = 0; t < first_masked && t < n_tiles; ++t) sweep2_tile(t, std::false_type{});
+  for (int t = first_masked; t < n_tiles; ++t) sweep2_tile(t, std::true_type{});
+
+  // ---------------- output: O / sum, staged through LDS for 16-byte stores ----------------
+  if (active && h == 0) sm.il[wave][l32] = inv_l;
+  __syncthreads();
+  uint16_t* ost = reinterpret_cast<uint16_t*>(smem_raw) + static_cast<size_t>(wave) * kRowsWave * (D + kPadO);
+  if (active) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int r = 8 * (v >> 2) + 4 * h + (v & 3);
+      const float sc = sm.il[wave][r];
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        ost[r * (D + kPadO) + db * 32 + l32] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(o[db][v] * sc));
     }
   }
-
-  // ---------------- output ----------------
-  if (wave_active) {
+  __syncthreads();
+  if (active) {
     uint16_t* og = static_cast<uint16_t*>(a.out) + static_cast<size_t>(layer * a.H_q + g * a.G) * a.T * D;
 #pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) {
-      const int r = row0 + qb * 32 + l32;
-      if (r >= GT) continue;
-      uint16_t* orow = og + static_cast<size_t>(r) * D;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int vq = 0; vq < 4; ++vq) {
-          __bf16 w[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) w[u] = static_cast<__bf16>(o[qb][db][vq * 4 + u] * inv_l[qb]);
-          uint2 packed;
-          packed.x = static_cast<unsigned>(__builtin_bit_cast(uint16_t, w[0])) |
-                     (static_cast<unsigned>(__builtin_bit_cast(uint16_t, w[1])) << 16);
-          packed.y = static_cast<unsigned>(__builtin_bit_cast(uint16_t, w[2])) |
-                     (static_cast<unsigned>(__builtin_bit_cast(uint16_t, w[3])) << 16);
-          *reinterpret_cast<uint2*>(orow + db * 32 + vq * 8 + 4 * h) = packed;
-        }
-      }
+    for (int it = 0; it < kRowsWave * KCH / 64; ++it) {
+      const int idx = it * 64 + lane;
+      const int r = idx / KCH, ch = idx % KCH;
+      if (row0 + r < GT)
+        *reinterpret_cast<u32x4*>(og + static_cast<size_t>(row0 + r) * D + ch * 8) =
+            *reinterpret_cast<const u32x4*>(ost + r * (D + kPadO) + ch * 8);
     }
   }
 }
@@ -401,9 +357,9 @@ hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream
   const int n_work = a.n_layers * a.H_kv * a.n_qtiles;
   const int grid = ((n_work + 7) / 8) * 8;
   if (head_dim == 128) {
-    hipLaunchKernelGGL(attn_mfma_kernel<128>, dim3(grid), dim3(256), sizeof(Smem<128>), s, a);
+    hipLaunchKernelGGL(attn_mfma_kernel<128>, dim3(grid), dim3(kThreads), sizeof(Smem<128>), s, a);
   } else {
-    hipLaunchKernelGGL(attn_mfma_kernel<64>, dim3(grid), dim3(256), sizeof(Smem<64>), s, a);
+    hipLaunchKernelGGL(attn_mfma_kernel<64>, dim3(grid), dim3(kThreads), sizeof(Smem<64>), s, a);
   }
   return hipGetLastError();
 }
