@@ -13,9 +13,11 @@
 //     same K/V).  Two waves per SIMD let the hardware run one wave's exp/softmax
 //     VALU work under the other wave's MFMAs; a single wave does not overlap its
 //     own MFMA and VALU streams well on gfx950.
-//   * Keys stream through LDS in tiles of 64 (two 32-key blocks), double
+//   * Keys stream through LDS in tiles of 128 (four 32-key blocks), double
 //     buffered, K and V both row-major; the next tile's global loads are issued
-//     before the current tile's compute.
+//     before the current tile's compute.  A block's K (and V) operand reads are
+//     all issued before its MFMA chain, and waves raise their priority while
+//     issuing MFMAs so the other wave on the SIMD fills the VALU slots.
 //   * Two sweeps over the keys.  Sweep 1: S^T = K Q^T -> per-row max and sum of
 //     exp2.  Sweep 2: S^T again -> E = exp2(x - row max) -> O += E V (scaled by
 //     1/sum at the end) and per-key column sums of P = E / sum.  Exact
@@ -53,7 +55,7 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kRowsWave = 32;
-constexpr int kKT = 64;        // keys per LDS tile (two 32-key blocks)
+constexpr int kKT = 128;       // keys per LDS tile (four 32-key blocks)
 constexpr int kPadK = 8;       // K row padding (bf16): 16-byte reads conflict-free
 constexpr int kPadV = 16;      // V row padding (bf16): transpose reads conflict-free
 constexpr int kPadO = 8;       // output staging row padding (bf16)
@@ -195,12 +197,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
 
   // S^T block (32 keys x 32 rows) for key block kb of buffer b.
   auto qk = [&](int b, int kb) -> f32x16 {
+    __builtin_amdgcn_s_setprio(1);
+    u32x4 kop[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kop[ks] = *reinterpret_cast<const u32x4*>(&sm.k[b][kb * 32 + l32][ks * 16 + h * 8]);
     f32x16 acc = {};
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const u32x4 x = *reinterpret_cast<const u32x4*>(&sm.k[b][kb * 32 + l32][ks * 16 + h * 8]);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, x), qreg[ks], acc, 0, 0, 0);
-    }
+    for (int ks = 0; ks < KS; ++ks)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kop[ks]), qreg[ks], acc, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < KS; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+#pragma unroll
+    for (int i = 0; i < KS; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    __builtin_amdgcn_s_setprio(0);
     return acc;
   };
 
@@ -211,7 +220,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (t + 1 < n_tiles) load_tile(t + 1, false);
     if (active) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < kKT / 32; ++kb) {
         const f32x16 acc = qk(b, kb);
         float z[16];
 #pragma unroll
@@ -274,7 +283,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (t + 1 < n_tiles) load_tile(t + 1, true);
     if (active) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < kKT / 32; ++kb) {
         const f32x16 acc = qk(b, kb);
         const int rel = lim - (t * kKT + kb * 32 + 4 * h);
         bf16x8 pe[2];
@@ -288,6 +297,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
           pe[v >> 3][v & 7] = static_cast<__bf16>(e);
           cs[v] = e * inv_l;
         }
+        __builtin_amdgcn_s_setprio(1);
+        bf16x8 vop[2][DB];
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
           const int r = kb * 32 + s * 16 + tr_row;
@@ -295,15 +306,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
           for (int db = 0; db < DB; ++db) {
             const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(&sm.v[b][r][db * 32 + tr_col]));
             const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(&sm.v[b][r + 8][db * 32 + tr_col]));
-            const bf16x8 vb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pe[s], vb, o[db], 0, 0, 0);
+            vop[s][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
           }
         }
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+          for (int db = 0; db < DB; ++db) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pe[s], vop[s][db], o[db], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4 * DB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+#pragma unroll
+        for (int i = 0; i < 2 * DB; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+        __builtin_amdgcn_s_setprio(0);
         const float tot = column_reduce(cs, lane);
         if ((lane & 1) == 0) sm.cs[b][wave][kb * 32 + key_lane] = tot;
       }
     } else {
-      sm.cs[b][wave][lane] = 0.f;
+      for (int i = lane; i < kKT; i += 64) sm.cs[b][wave][i] = 0.f;
     }
     if (t + 1 < n_tiles) store_tile(b ^ 1, true);
     __syncthreads();
