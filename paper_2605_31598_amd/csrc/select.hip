@@ -3,13 +3,14 @@
 // 1. Finalise the importance scores of the candidate pool (state slots, then the
 //    frame's tokens): s_j = (1/T) * sum over row tiles of the attention kernel's
 //    column sums, added in fixed tile order (deterministic, no atomics).
-// 2. If the pool exceeds B, find the B-th largest composite key
-//    (float bits of s) << 32 | (0xFFFFFFFF - position) with an 8-pass, 8-bit radix
-//    select over the pool held in LDS.  Scores are non-negative, so their IEEE
-//    bits order like the values; the low word makes the lower position win on
-//    equal scores.  Composite keys of distinct positions are distinct, so exactly
-//    B keys are >= the threshold.
-// 3. Pair evicted state slots (then free slots S, S+1, ...) with admitted frame
+// 2. If the pool exceeds B, find the threshold score s* = the B-th largest score
+//    with a radix select over the fp32 bit patterns (non-negative floats order
+//    like their bits).  Digits start below the common leading bits of the pool's
+//    minimum and maximum, so no pass puts every key into one histogram bin.
+// 3. Entries with s > s* are kept; among entries with s == s* (exact ties) the
+//    lowest positions fill the remaining places, found by a second radix select
+//    over the tied entries' positions (only when the ties straddle the boundary).
+// 4. Pair evicted state slots (then free slots S, S+1, ...) with admitted frame
 //    tokens in ascending order using block-wide scans.  The state update kernel
 //    copies the admitted rows; retained slots never move.
 #include "internal.h"
@@ -17,11 +18,6 @@
 namespace skv {
 
 namespace {
-
-__device__ inline uint64_t composite_key(float s, int32_t pos) {
-  return (static_cast<uint64_t>(__float_as_uint(s)) << 32) |
-         static_cast<uint64_t>(0xFFFFFFFFu - static_cast<uint32_t>(pos));
-}
 
 // Exclusive prefix count of `flag` over the workgroup; *total receives the sum.
 __device__ inline int block_exclusive_count(bool flag, int* wave_count, int* total) {
@@ -43,19 +39,137 @@ __device__ inline int block_exclusive_count(bool flag, int* wave_count, int* tot
   return before + within;
 }
 
+struct SelectShared {
+  uint32_t hist[256];
+  uint32_t wave_min[kSelectThreads / 64];
+  uint32_t wave_max[kSelectThreads / 64];
+  int wave_count[kSelectThreads / 64];
+  uint32_t lo, hi, count;
+  int remaining;
+  int digit;
+};
+
+struct RadixResult {
+  uint32_t value;  // the rank-th largest key
+  int need;        // how many entries equal to `value` fall within the top `rank`
+  int equal;       // how many active entries equal `value`
+};
+
+__device__ inline uint32_t wave_min_u32(uint32_t x) {
+  for (int off = 32; off > 0; off >>= 1) x = min(x, static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), off, 64)));
+  return x;
+}
+__device__ inline uint32_t wave_max_u32(uint32_t x) {
+  for (int off = 32; off > 0; off >>= 1) x = max(x, static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), off, 64)));
+  return x;
+}
+__device__ inline int wave_sum_i32(int x) {
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+
+// Radix select over the active entries j < n: the rank-th largest key
+// (1 <= rank <= number of active entries).  Digits of 8 bits start below the
+// leading bits that all active keys share.
+template <typename KeyFn, typename ActiveFn>
+__device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active, SelectShared& sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_waves = blockDim.x >> 6;
+  uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+  int cnt = 0;
+  for (int j = tid; j < n; j += blockDim.x) {
+    if (active(j)) {
+      const uint32_t k = key(j);
+      lo = min(lo, k);
+      hi = max(hi, k);
+      ++cnt;
+    }
+  }
+  lo = wave_min_u32(lo);
+  hi = wave_max_u32(hi);
+  cnt = wave_sum_i32(cnt);
+  if (lane == 0) {
+    sh.wave_min[wave] = lo;
+    sh.wave_max[wave] = hi;
+    sh.wave_count[wave] = cnt;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t l = 0xFFFFFFFFu, h = 0u, c = 0u;
+    for (int w = 0; w < n_waves; ++w) {
+      l = min(l, sh.wave_min[w]);
+      h = max(h, sh.wave_max[w]);
+      c += static_cast<uint32_t>(sh.wave_count[w]);
+    }
+    sh.lo = l;
+    sh.hi = h;
+    sh.count = c;
+  }
+  __syncthreads();
+  const uint32_t any_key = sh.hi;
+  const uint32_t diff = sh.lo ^ sh.hi;
+  const int n_active = static_cast<int>(sh.count);
+  __syncthreads();
+  if (diff == 0u) return {any_key, rank, n_active};  // all active keys are equal
+
+  const int top_bit = 31 - __clz(static_cast<int>(diff));  // highest bit where active keys differ
+  uint32_t prefix = top_bit == 31 ? 0u : (any_key >> (top_bit + 1)) << (top_bit + 1);
+  int remaining = rank;
+  int equal = n_active;
+  for (int shift = top_bit + 1; shift > 0;) {
+    const int width = shift >= 8 ? 8 : shift;
+    shift -= width;
+    const uint32_t dmask = (1u << width) - 1u;
+    const uint32_t fixed = ~((dmask << shift) | ((1u << shift) - 1u));  // bits already decided
+    for (int i = tid; i < 256; i += blockDim.x) sh.hist[i] = 0u;
+    __syncthreads();
+    for (int j = tid; j < n; j += blockDim.x) {
+      if (!active(j)) continue;
+      const uint32_t k = key(j);
+      if ((k & fixed) == prefix) atomicAdd(&sh.hist[(k >> shift) & dmask], 1u);
+    }
+    __syncthreads();
+    if (tid < 64) {
+      uint32_t c[4];
+      for (int b = 0; b < 4; ++b) c[b] = sh.hist[4 * tid + b];
+      const uint32_t mine = c[0] + c[1] + c[2] + c[3];
+      uint32_t suffix = mine;  // sum over lanes >= tid
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = __shfl_down(suffix, off, 64);
+        if (tid + off < 64) suffix += o;
+      }
+      uint32_t above = suffix - mine;  // keys in higher bins
+      for (int b = 3; b >= 0; --b) {
+        if (above < static_cast<uint32_t>(remaining) && static_cast<uint32_t>(remaining) <= above + c[b]) {
+          sh.digit = 4 * tid + b;
+          sh.remaining = remaining - static_cast<int>(above);
+          sh.count = c[b];
+        }
+        above += c[b];
+      }
+    }
+    __syncthreads();
+    prefix |= static_cast<uint32_t>(sh.digit) << shift;
+    remaining = sh.remaining;
+    equal = static_cast<int>(sh.count);
+    __syncthreads();
+  }
+  return {prefix, remaining, equal};
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelectArgs a) {
-  extern __shared__ uint64_t pool_key[];
-  __shared__ uint32_t hist[256];
-  __shared__ int wave_count[kSelectThreads / 64];
-  __shared__ int sh_digit, sh_remaining;
+  extern __shared__ uint32_t pool_mem[];  // [pool] score bits, then [pool] positions
+  __shared__ SelectShared sh;
 
   const int lg = blockIdx.x;
   const int tid = threadIdx.x;
   const int S = a.S, T = a.T, B = a.B, P = S + T;
+  uint32_t* sbits = pool_mem;
+  int32_t* spos = reinterpret_cast<int32_t*>(pool_mem + P);
   const float* part = a.partial + static_cast<size_t>(lg) * a.n_qtiles * a.pool_stride;
-  const int32_t* spos = a.state_pos + static_cast<size_t>(lg) * B;
+  const int32_t* state_pos = a.state_pos + static_cast<size_t>(lg) * B;
   float* sscore = a.state_score + static_cast<size_t>(lg) * B;
   float* pscore = a.pool_score + static_cast<size_t>(lg) * a.pool_stride;
   int32_t* ppos = a.pool_pos + static_cast<size_t>(lg) * a.pool_stride;
@@ -66,61 +180,43 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelectArgs a) {
     float acc = 0.f;
     for (int t = 0; t < a.n_qtiles; ++t) acc += part[static_cast<size_t>(t) * a.pool_stride + j];
     const float s = acc * a.inv_T;
-    const int32_t pos = j < S ? spos[j] : a.frame_pos0 + (j - S);
+    const int32_t pos = j < S ? state_pos[j] : a.frame_pos0 + (j - S);
     pscore[j] = s;
     ppos[j] = pos;
-    pool_key[j] = composite_key(s, pos);
+    sbits[j] = __float_as_uint(s);
+    spos[j] = pos;
   }
   __syncthreads();
 
   const bool prune = P > B;
-  uint64_t thr = 0;
+  uint32_t s_thr = 0u;  // keep s > s_thr, and s == s_thr with position <= p_thr
+  int32_t p_thr = 0x7FFFFFFF;
   if (prune && B > 0) {
-    uint64_t prefix = 0;
-    int remaining = B;  // rank (from the top) of the wanted key among keys matching `prefix`
-    for (int pass = 0; pass < 8; ++pass) {
-      const int shift = 56 - 8 * pass;
-      for (int i = tid; i < 256; i += blockDim.x) hist[i] = 0u;
-      __syncthreads();
-      for (int j = tid; j < P; j += blockDim.x) {
-        const uint64_t k = pool_key[j];
-        const bool match = pass == 0 || ((k ^ prefix) >> (shift + 8)) == 0;
-        if (match) atomicAdd(&hist[(k >> shift) & 255u], 1u);
-      }
-      __syncthreads();
-      if (tid < 64) {
-        uint32_t c[4];
-        for (int b = 0; b < 4; ++b) c[b] = hist[4 * tid + b];
-        const uint32_t mine = c[0] + c[1] + c[2] + c[3];
-        uint32_t suffix = mine;  // sum over lanes >= tid
-        for (int off = 1; off < 64; off <<= 1) {
-          const uint32_t o = __shfl_down(suffix, off, 64);
-          if (tid + off < 64) suffix += o;
-        }
-        uint32_t above = suffix - mine;  // keys in higher bins
-        for (int b = 3; b >= 0; --b) {
-          if (above < static_cast<uint32_t>(remaining) && static_cast<uint32_t>(remaining) <= above + c[b]) {
-            sh_digit = 4 * tid + b;
-            sh_remaining = remaining - static_cast<int>(above);
-          }
-          above += c[b];
-        }
-      }
-      __syncthreads();
-      prefix |= static_cast<uint64_t>(sh_digit) << shift;
-      remaining = sh_remaining;
-      __syncthreads();
+    const RadixResult r = radix_select(P, B, [&](int j) { return sbits[j]; }, [&](int) { return true; }, sh);
+    s_thr = r.value;
+    if (r.need < r.equal) {
+      // exact ties straddle the boundary: the r.need lowest positions among s == s_thr;
+      // a complemented position makes "largest" mean "lowest position"
+      const RadixResult q = radix_select(
+          P, r.need, [&](int j) { return 0x7FFFFFFFu - static_cast<uint32_t>(spos[j]); },
+          [&](int j) { return sbits[j] == s_thr; }, sh);
+      p_thr = static_cast<int32_t>(0x7FFFFFFFu - q.value);
     }
-    thr = prefix;
   }
+  auto kept = [&](int j) -> bool {
+    if (!prune) return true;
+    if (B == 0) return false;
+    const uint32_t s = sbits[j];
+    return s > s_thr || (s == s_thr && spos[j] <= p_thr);
+  };
 
   // Admitted frame tokens, ascending t.
   int n_adm = 0;
   for (int base = 0; base < T; base += blockDim.x) {
     const int t = base + tid;
-    const bool adm = t < T && (!prune || (B > 0 && pool_key[S + t] >= thr));
+    const bool adm = t < T && kept(S + t);
     int tot;
-    const int rank = block_exclusive_count(adm, wave_count, &tot);
+    const int rank = block_exclusive_count(adm, sh.wave_count, &tot);
     if (adm) asrc[n_adm + rank] = t;
     n_adm += tot;
   }
@@ -128,10 +224,10 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelectArgs a) {
   int n_ev = 0;
   for (int base = 0; base < S; base += blockDim.x) {
     const int j = base + tid;
-    const bool ev = j < S && prune && (B == 0 || pool_key[j] < thr);
-    if (j < S && !ev) sscore[j] = pscore[j];
+    const bool ev = j < S && !kept(j);
+    if (j < S && !ev) sscore[j] = __uint_as_float(sbits[j]);
     int tot;
-    const int rank = block_exclusive_count(ev, wave_count, &tot);
+    const int rank = block_exclusive_count(ev, sh.wave_count, &tot);
     if (ev) adst[n_ev + rank] = j;
     n_ev += tot;
   }
@@ -145,7 +241,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelectArgs a) {
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-  const size_t lds = static_cast<size_t>(a.S + a.T) * sizeof(uint64_t);
+  const size_t lds = static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t);
   hipLaunchKernelGGL(select_kernel, dim3(a.n_layers * a.H_kv), dim3(kSelectThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -153,7 +249,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
 hipError_t prepare_select(int pool_stride) {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                             static_cast<int>(pool_stride * sizeof(uint64_t)));
+                             static_cast<int>(pool_stride * 2 * sizeof(uint32_t)));
 }
 
 }  // namespace skv
