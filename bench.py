@@ -34,10 +34,15 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_mfma_vlm7b_28layer_traffic.t
 
 
 def attn_source_hash():
+    """Hash of what the attention kernel is built from: its source file and the
+    launch-argument struct it reads (the rest of internal.h serves other kernels)."""
     h = hashlib.sha256()
-    for p in ATTN_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+    with open(os.path.join(ROOT, ATTN_SOURCES[0]), "rb") as f:
+        h.update(f.read())
+    with open(os.path.join(ROOT, ATTN_SOURCES[1]), "r") as f:
+        text = f.read()
+    start = text.index("struct AttnArgs {")
+    h.update(text[start:text.index("};", start) + 2].encode())
     return h.hexdigest()[:16]
 
 
@@ -66,23 +71,27 @@ def attention_flops(wl, S):
 
 
 def executed_mfma_flops(wl, S):
-    """MFMA FLOPs the kernel issues: two sweeps of K Q^T plus one V^T P^T over whole tiles
-    (64-row waves, 64-key tiles)."""
-    rows = wl.group * wl.tokens_per_frame
-    waves = -(-rows // 64)
-    keys = -(-(S + wl.tokens_per_frame) // 64) * 64
-    return 3 * 2 * (waves * 64) * keys * wl.head_dim * wl.n_kv_heads * wl.n_layers
+    """MFMA FLOPs the attention kernel issues: K Q^T in both sweeps plus P V once, over
+    whole 32-row wave blocks and 128-key tiles."""
+    T = wl.tokens_per_frame
+    rows = -(-(wl.group * T) // 32) * 32
+    keys = -(-(S + T) // 128) * 128
+    return 3 * 2 * rows * keys * wl.head_dim * wl.n_kv_heads * wl.n_layers
 
 
-def stage_bytes(wl, S, n_qtiles):
-    """Algorithmic HBM bytes per launch of the select, update and append stages."""
+def refresh_bytes(wl, S, n_qtiles, admitted):
+    """Algorithmic HBM bytes of one refresh launch: score finalisation and selection
+    (column-sum partials and state positions read; pool scores/positions, retained
+    scores and admit lists written), the admitted rows' K/V copied into the state
+    (read + write, plus position and score), and the frame's K/V appended to the
+    decode cache (read + write).  `admitted` = mean admitted rows per (layer, KV head)."""
     LH = wl.n_layers * wl.n_kv_heads
     T, rb = wl.tokens_per_frame, wl.head_dim * 2
     P = S + T
     select = LH * (n_qtiles * P * 4 + S * 4 + P * 8 + 2 * T * 4 + S * 4)
-    update_worst = LH * min(T, wl.capacity) * (2 * 2 * rb + 8)  # admitted rows: read + write K and V
+    update = LH * admitted * (2 * 2 * rb + 8)
     append = LH * T * rb * 2 * 2
-    return select, update_worst, append
+    return select + update + append
 
 
 def cpu_baseline(wl, seconds):
@@ -201,7 +210,10 @@ def main():
     run(args.steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    stages = st.timing_stop(args.steps)  # [K, 4] ms
+    stages = st.timing_stop(args.steps)  # [K, 2] ms: attention, refresh
+    # rows admitted by the last timed frame (its positions are the newest in the state)
+    last_pos0 = wl.pos_offset + ((counter["i"] - 1) % N) * T
+    admitted = float(np.mean([(st.read_state(l)["pos"] >= last_pos0).sum(axis=1).mean() for l in range(L)]))
     st.close()
     elapsed = t1 - t0
     fps = args.steps / elapsed
@@ -215,10 +227,8 @@ def main():
     achieved = alg.sum() / (attn_ms.sum() * 1e-3) / 1e12
     executed = exe.sum() / (attn_ms.sum() * 1e-3) / 1e12
     n_qtiles = -(-(wl.group * T) // 256)
-    sel_b, upd_b, app_b = (np.array([stage_bytes(wl, int(s), n_qtiles)[i] for s in S]) for i in range(3))
-
-    def gbs(b, col):
-        return float(b.sum() / (stages[:, col].astype(np.float64).sum() * 1e-3) / 1e9)
+    ref_b = np.array([refresh_bytes(wl, int(s), n_qtiles, admitted) for s in S], dtype=np.float64)
+    refresh_gbs = float(ref_b.sum() / (stages[:, 1].astype(np.float64).sum() * 1e-3) / 1e9)
 
     frame_ms = stages.sum(axis=1)
     full = frames >= wl.full_from_frame
@@ -258,12 +268,12 @@ def main():
             "executed_mfma_tflops": round(executed, 2),
             "executed_frac": round(executed / PEAK_BF16_TFLOPS, 4),
         },
-        "stages_ms_mean": {n: float(stages[:, i].mean()) for i, n in enumerate(("attention", "select", "update",
-                                                                                  "append"))},
+        "stages_ms_mean": {n: float(stages[:, i].mean()) for i, n in enumerate(("attention", "refresh"))},
         "hbm": {
-            "select_GBps": round(gbs(sel_b, 1), 1),
-            "update_GBps_at_T_admitted": round(gbs(upd_b, 2), 1),
-            "append_GBps": round(gbs(app_b, 3), 1),
+            "kernel": "refresh_kernel (selection + state update + decode-cache append)",
+            "bytes_per_launch": float(ref_b.mean()),
+            "admitted_rows_per_head": round(admitted, 1),
+            "GBps": round(refresh_gbs, 1),
             "peak_GBps": PEAK_HBM_GBS,
         },
         "latency": {

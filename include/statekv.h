@@ -137,11 +137,12 @@ skv_status skv_seek(skv_ctx* ctx, int64_t frame);
 /* Kernel timing with HIP events on the context's stream.  skv_timing_start
  * creates events for up to max_steps subsequent skv_frame_step calls (created
  * here, never in the step).  skv_timing_stop synchronises the stream and
- * writes ms[i * SKV_N_STAGES + s] for step i and stage s (attention, selection,
- * state update, cache append), *n_steps the number of steps recorded, then
- * releases the events. */
-enum { SKV_STAGE_ATTENTION = 0, SKV_STAGE_SELECT = 1, SKV_STAGE_UPDATE = 2, SKV_STAGE_APPEND = 3,
-       SKV_N_STAGES = 4 };
+ * writes ms[i * SKV_N_STAGES + s] for step i and stage s, *n_steps the number
+ * of steps recorded, then releases the events.  Stages: the attention launch
+ * (attention and column sums of P), and the refresh launch (score
+ * finalisation, Top-B selection and state update, with the decode-cache append
+ * running in the same launch). */
+enum { SKV_STAGE_ATTENTION = 0, SKV_STAGE_REFRESH = 1, SKV_N_STAGES = 2 };
 skv_status skv_timing_start(skv_ctx* ctx, int32_t max_steps);
 skv_status skv_timing_stop(skv_ctx* ctx, int32_t* n_steps, float* ms, int32_t ms_capacity);
 

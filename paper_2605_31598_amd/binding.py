@@ -25,8 +25,8 @@ SKV_ERR_UNSUPPORTED = -6
 
 SKV_BF16 = 0
 SKV_F32 = 1
-N_STAGES = 4
-STAGES = ("attention", "select", "update", "append")
+N_STAGES = 2
+STAGES = ("attention", "refresh")
 
 # Every symbol declared in include/statekv.h.
 EXPORTS = (

@@ -22,45 +22,29 @@ struct AttnArgs {
   float scale_log2;    // softmax scale * log2(e)
 };
 
-struct SelectArgs {
-  const float* partial;  // as in AttnArgs
+// The refresh launch finishes a frame for `n_layers` layers: score finalisation,
+// Top-B selection and state update in one workgroup per (layer, KV head), the
+// decode-cache append in a second set of workgroups of the same grid.
+struct RefreshArgs {
+  const float* partial;      // as in AttnArgs
   int n_qtiles, pool_stride;
-  const int32_t* state_pos;  // [n_layers][H_kv][B]
+  const void* kf;            // [n_layers][H_kv][T][d]   frame keys
+  const void* vf;            //                          frame values
+  void* ks;                  // [n_layers][H_kv][B][d]   state slots
+  void* vs;
+  int32_t* state_pos;        // [n_layers][H_kv][B]
   float* state_score;        // [n_layers][H_kv][B]
   float* pool_score;         // [n_layers][H_kv][pool_stride]
   int32_t* pool_pos;         // [n_layers][H_kv][pool_stride]
   int32_t* admit_src;        // [n_layers][H_kv][T]  frame token of the a-th admitted candidate
   int32_t* admit_dst;        // [n_layers][H_kv][T]  state slot it goes to
-  int32_t* admit_count;      // [n_layers][H_kv]
+  void* ck;                  // [n_layers][H_kv][max_tokens][d]  decode cache
+  void* cv;
+  int64_t max_tokens, first_row;  // first_row = frame * T
   int n_layers, H_kv, T, B, S;
+  int row_bytes;             // d * element size, a multiple of 16
   int32_t frame_pos0;        // virtual position of frame token 0
   float inv_T;
-};
-
-struct UpdateArgs {
-  const void* kf;            // [n_layers][H_kv][T][d]
-  const void* vf;
-  void* ks;                  // [n_layers][H_kv][B][d]
-  void* vs;
-  int32_t* state_pos;        // [n_layers][H_kv][B]
-  float* state_score;
-  const float* pool_score;   // [n_layers][H_kv][pool_stride]
-  const int32_t* admit_src;
-  const int32_t* admit_dst;
-  const int32_t* admit_count;
-  int n_layers, H_kv, T, B, S, pool_stride;
-  int row_bytes;             // d * element size, a multiple of 16
-  int32_t frame_pos0;
-};
-
-struct AppendArgs {
-  const void* kf;            // [n_layers][H_kv][T][d]
-  const void* vf;
-  void* ck;                  // [n_layers][H_kv][max_tokens][d]
-  void* cv;
-  int n_layers, H_kv, T;
-  int64_t max_tokens, first_row;  // first_row = frame * T
-  int row_bytes;
 };
 
 constexpr int kMfmaRowsPerTile = 256;   // query rows (G*T packed) per attention workgroup
@@ -70,9 +54,7 @@ constexpr int kMaxPool = 16384;         // B + T limit (selection keeps the pool
 
 hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s);
-hipError_t launch_select(const SelectArgs& a, hipStream_t s);
-hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
-hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s);
 hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride);
 
 }  // namespace skv

@@ -1,5 +1,6 @@
-// Top-B refresh of the compressed state (Eq. 6), one workgroup per (layer, KV head).
+// Frame refresh (Eq. 4 and Eq. 6): one launch, two kinds of workgroup.
 //
+// Workgroups 0 .. L*H_kv-1, one per (layer, KV head), refresh the compressed state:
 // 1. Finalise the importance scores of the candidate pool (state slots, then the
 //    frame's tokens): s_j = (1/T) * sum over row tiles of the attention kernel's
 //    column sums, added in fixed tile order (deterministic, no atomics).
@@ -11,8 +12,10 @@
 //    lowest positions fill the remaining places, found by a second radix select
 //    over the tied entries' positions (only when the ties straddle the boundary).
 // 4. Pair evicted state slots (then free slots S, S+1, ...) with admitted frame
-//    tokens in ascending order using block-wide scans.  The state update kernel
-//    copies the admitted rows; retained slots never move.
+//    tokens in ascending order using block-wide scans, then copy the admitted
+//    K/V rows into those slots.  Retained slots never move.
+// Workgroups L*H_kv .. 2*L*H_kv-1 append the frame's K/V rows of one (layer, KV
+// head) to the decode cache D (the detailed state), concurrently with the above.
 #include "internal.h"
 
 namespace skv {
@@ -157,19 +160,20 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
   return {prefix, remaining, equal};
 }
 
-}  // namespace
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(kSelectThreads) void select_kernel(SelectArgs a) {
-  extern __shared__ uint32_t pool_mem[];  // [pool] score bits, then [pool] positions
-  __shared__ SelectShared sh;
+__device__ inline void copy16(const void* src, void* dst, size_t off) {
+  *reinterpret_cast<u32x4*>(static_cast<char*>(dst) + off) =
+      *reinterpret_cast<const u32x4*>(static_cast<const char*>(src) + off);
+}
 
-  const int lg = blockIdx.x;
+__device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, uint32_t* pool_mem) {
   const int tid = threadIdx.x;
   const int S = a.S, T = a.T, B = a.B, P = S + T;
   uint32_t* sbits = pool_mem;
   int32_t* spos = reinterpret_cast<int32_t*>(pool_mem + P);
   const float* part = a.partial + static_cast<size_t>(lg) * a.n_qtiles * a.pool_stride;
-  const int32_t* state_pos = a.state_pos + static_cast<size_t>(lg) * B;
+  int32_t* state_pos = a.state_pos + static_cast<size_t>(lg) * B;
   float* sscore = a.state_score + static_cast<size_t>(lg) * B;
   float* pscore = a.pool_score + static_cast<size_t>(lg) * a.pool_stride;
   int32_t* ppos = a.pool_pos + static_cast<size_t>(lg) * a.pool_stride;
@@ -237,17 +241,65 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelectArgs a) {
   const int n_holes = n_ev + (B - S);
   const int count = n_adm < n_holes ? n_adm : n_holes;
   for (int i = n_ev + tid; i < count; i += blockDim.x) adst[i] = S + (i - n_ev);
-  if (tid == 0) a.admit_count[lg] = count;
+  __syncthreads();  // the admit lists are read back by other threads below
+
+  // State update: admitted frame rows into their slots, 16-byte chunks.
+  const int chunks = a.row_bytes >> 4;
+  const size_t src_base = static_cast<size_t>(lg) * T * a.row_bytes;
+  const size_t dst_base = static_cast<size_t>(lg) * B * a.row_bytes;
+  for (int idx = tid; idx < count * chunks; idx += blockDim.x) {
+    const int i = idx / chunks;
+    const int c = idx - i * chunks;
+    const int src = asrc[i], dst = adst[i];
+    const size_t so = src_base + static_cast<size_t>(src) * a.row_bytes + (static_cast<size_t>(c) << 4);
+    const size_t dof = dst_base + static_cast<size_t>(dst) * a.row_bytes + (static_cast<size_t>(c) << 4);
+    *reinterpret_cast<u32x4*>(static_cast<char*>(a.ks) + dof) =
+        *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.kf) + so);
+    *reinterpret_cast<u32x4*>(static_cast<char*>(a.vs) + dof) =
+        *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.vf) + so);
+    if (c == 0) {
+      state_pos[dst] = a.frame_pos0 + src;
+      sscore[dst] = __uint_as_float(sbits[S + src]);
+    }
+  }
 }
 
-hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+// Decode-cache append of one (layer, KV head): T contiguous rows of K and V.
+__device__ void append_frame(const RefreshArgs& a, int lg) {
+  const size_t bytes = static_cast<size_t>(a.T) * a.row_bytes;
+  const size_t src = static_cast<size_t>(lg) * bytes;
+  const size_t dst = (static_cast<size_t>(lg) * a.max_tokens + a.first_row) * a.row_bytes;
+  const char* kf = static_cast<const char*>(a.kf) + src;
+  const char* vf = static_cast<const char*>(a.vf) + src;
+  char* ck = static_cast<char*>(a.ck) + dst;
+  char* cv = static_cast<char*>(a.cv) + dst;
+  for (size_t off = static_cast<size_t>(threadIdx.x) << 4; off < bytes; off += static_cast<size_t>(blockDim.x) << 4) {
+    copy16(kf, ck, off);
+    copy16(vf, cv, off);
+  }
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kSelectThreads) void refresh_kernel(RefreshArgs a) {
+  extern __shared__ uint32_t pool_mem[];  // [pool] score bits, then [pool] positions
+  __shared__ SelectShared sh;
+  const int n_lg = a.n_layers * a.H_kv;
+  if (static_cast<int>(blockIdx.x) < n_lg) {
+    refresh_state(a, blockIdx.x, sh, pool_mem);
+  } else {
+    append_frame(a, blockIdx.x - n_lg);
+  }
+}
+
+hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s) {
   const size_t lds = static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t);
-  hipLaunchKernelGGL(select_kernel, dim3(a.n_layers * a.H_kv), dim3(kSelectThreads), lds, s, a);
+  hipLaunchKernelGGL(refresh_kernel, dim3(2 * a.n_layers * a.H_kv), dim3(kSelectThreads), lds, s, a);
   return hipGetLastError();
 }
 
-hipError_t prepare_select(int pool_stride) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
+hipError_t prepare_refresh(int pool_stride) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(refresh_kernel),
                              hipFuncAttributeMaxDynamicSharedMemorySize,
                              static_cast<int>(pool_stride * 2 * sizeof(uint32_t)));
 }

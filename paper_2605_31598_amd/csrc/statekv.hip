@@ -1,11 +1,12 @@
 // Host runtime of the StateKV frame step: configuration checks, one-time device
 // allocation, per-frame launch sequence and the C ABI of include/statekv.h.
 //
-// Per frame and layer range the stream receives, in order:
+// Per frame and layer range the stream receives two launches:
 //   1. attention + fused column sums of P     (Eq. 5 and the importance score)
-//   2. score finalisation + Top-B selection   (Eq. 6, ties to the lowest position)
-//   3. state update: admitted rows into evicted or free slots
-//   4. decode-cache append of the frame's K/V (Eq. 4, detailed state)
+//   2. refresh: score finalisation, Top-B selection (Eq. 6, ties to the lowest
+//      position) and the state update (admitted rows into evicted or free
+//      slots), concurrently with the decode-cache append of the frame's K/V
+//      (Eq. 4, detailed state)
 // The state size S_n = min(B, n * T) and the frame's virtual positions
 // L_n + t are host-side bookkeeping (virtual sequence length paragraph), so the
 // step needs no device-to-host synchronisation.
@@ -21,7 +22,7 @@
 #include "internal.h"
 
 namespace skv {
-hipError_t prepare_select(int pool_stride);
+hipError_t prepare_refresh(int pool_stride);
 hipError_t prepare_attention_mfma();
 }  // namespace skv
 
@@ -66,7 +67,6 @@ struct skv_ctx {
   int32_t* pool_pos = nullptr;
   int32_t* admit_src = nullptr;    // [L][H_kv][T]
   int32_t* admit_dst = nullptr;
-  int32_t* admit_count = nullptr;  // [L][H_kv]
   std::vector<void*> allocations;
 
   // progress of the stream
@@ -192,7 +192,6 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
       {reinterpret_cast<void**>(&ctx->pool_pos), LH * ctx->pool_stride * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_src), LH * c.tokens_per_frame * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_dst), LH * c.tokens_per_frame * sizeof(int32_t)},
-      {reinterpret_cast<void**>(&ctx->admit_count), LH * sizeof(int32_t)},
   };
   for (const Req& r : reqs) {
     const skv_status s = alloc(ctx, r.bytes, r.p);
@@ -253,68 +252,40 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.pool_stride = ctx->pool_stride;
   aa.scale_log2 = ctx->scale_log2;
 
-  skv::SelectArgs sa;
-  sa.partial = aa.partial;
-  sa.n_qtiles = ctx->n_qtiles;
-  sa.pool_stride = ctx->pool_stride;
-  sa.state_pos = ctx->state_pos + lh0 * B;
-  sa.state_score = ctx->state_score + lh0 * B;
-  sa.pool_score = ctx->pool_score + lh0 * ctx->pool_stride;
-  sa.pool_pos = ctx->pool_pos + lh0 * ctx->pool_stride;
-  sa.admit_src = ctx->admit_src + lh0 * T;
-  sa.admit_dst = ctx->admit_dst + lh0 * T;
-  sa.admit_count = ctx->admit_count + lh0;
-  sa.n_layers = layer_count;
-  sa.H_kv = Hkv;
-  sa.T = T;
-  sa.B = B;
-  sa.S = S;
-  sa.frame_pos0 = pos0;
-  sa.inv_T = 1.0f / static_cast<float>(T);
-
-  skv::UpdateArgs ua;
-  ua.kf = k;
-  ua.vf = v;
-  ua.ks = const_cast<void*>(aa.ks);
-  ua.vs = const_cast<void*>(aa.vs);
-  ua.state_pos = ctx->state_pos + lh0 * B;
-  ua.state_score = sa.state_score;
-  ua.pool_score = sa.pool_score;
-  ua.admit_src = sa.admit_src;
-  ua.admit_dst = sa.admit_dst;
-  ua.admit_count = sa.admit_count;
-  ua.n_layers = layer_count;
-  ua.H_kv = Hkv;
-  ua.T = T;
-  ua.B = B;
-  ua.S = S;
-  ua.pool_stride = ctx->pool_stride;
-  ua.row_bytes = static_cast<int>(rb);
-  ua.frame_pos0 = pos0;
-
-  skv::AppendArgs pa;
-  pa.kf = k;
-  pa.vf = v;
-  pa.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
-  pa.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
-  pa.n_layers = layer_count;
-  pa.H_kv = Hkv;
-  pa.T = T;
-  pa.max_tokens = ctx->max_tokens;
-  pa.first_row = ctx->frame * T;
-  pa.row_bytes = static_cast<int>(rb);
+  skv::RefreshArgs ra;
+  ra.partial = aa.partial;
+  ra.n_qtiles = ctx->n_qtiles;
+  ra.pool_stride = ctx->pool_stride;
+  ra.kf = k;
+  ra.vf = v;
+  ra.ks = static_cast<char*>(ctx->state_k) + lh0 * B * rb;
+  ra.vs = static_cast<char*>(ctx->state_v) + lh0 * B * rb;
+  ra.state_pos = ctx->state_pos + lh0 * B;
+  ra.state_score = ctx->state_score + lh0 * B;
+  ra.pool_score = ctx->pool_score + lh0 * ctx->pool_stride;
+  ra.pool_pos = ctx->pool_pos + lh0 * ctx->pool_stride;
+  ra.admit_src = ctx->admit_src + lh0 * T;
+  ra.admit_dst = ctx->admit_dst + lh0 * T;
+  ra.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
+  ra.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
+  ra.max_tokens = ctx->max_tokens;
+  ra.first_row = ctx->frame * T;
+  ra.n_layers = layer_count;
+  ra.H_kv = Hkv;
+  ra.T = T;
+  ra.B = B;
+  ra.S = S;
+  ra.row_bytes = static_cast<int>(rb);
+  ra.frame_pos0 = pos0;
+  ra.inv_T = 1.0f / static_cast<float>(T);
 
   hipError_t e = mark(0);
   if (e == hipSuccess)
     e = ctx->use_mfma ? skv::launch_attention_mfma_bf16(aa, d, ctx->stream)
                       : skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream);
   if (e == hipSuccess) e = mark(1);
-  if (e == hipSuccess) e = skv::launch_select(sa, ctx->stream);
+  if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
   if (e == hipSuccess) e = mark(2);
-  if (e == hipSuccess && B > 0) e = skv::launch_update(ua, ctx->stream);
-  if (e == hipSuccess) e = mark(3);
-  if (e == hipSuccess) e = skv::launch_append(pa, ctx->stream);
-  if (e == hipSuccess) e = mark(4);
   if (e != hipSuccess) return hip_fail(e, "frame step launch");
   if (timing) ++ctx->timing_n;
 
@@ -426,7 +397,7 @@ namespace skv {
 
 hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride) {
   (void)head_dim;
-  hipError_t e = prepare_select(pool_stride);
+  hipError_t e = prepare_refresh(pool_stride);
   if (e != hipSuccess) return e;
   if (bf16) e = prepare_attention_mfma();
   return e;
