@@ -18,7 +18,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = ["statekv.hip", "attn_mfma.hip", "attn_simple.hip", "refresh.hip"]
+SOURCES = ["statekv.hip", "attn_mfma.hip", "attn_simple.hip", "refresh.hip", "plan.cpp"]
 LIB = os.path.join(PKG, "libstatekv.so")
 GEN_SRC = os.path.join(ROOT, "workloads", "csrc", "skv_gen.hip")
 GEN_LIB = os.path.join(ROOT, "workloads", "libskvgen.so")
@@ -42,7 +42,7 @@ def _run(cmd):
 def build(verbose: bool = False) -> list:
     obj_dir = os.path.join(PKG, "_build")
     os.makedirs(obj_dir, exist_ok=True)
-    objs = [os.path.join(obj_dir, s.replace(".hip", ".o")) for s in SOURCES]
+    objs = [os.path.join(obj_dir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
     jobs = [[HIPCC, *FLAGS, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
     with cf.ThreadPoolExecutor(max_workers=min(len(jobs) + 1, 8)) as ex:
         futs = [ex.submit(_run, j) for j in jobs]

@@ -52,14 +52,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kWaves = 8;
+constexpr int kWaves = kMfmaWaves;
 constexpr int kThreads = kWaves * 64;
-constexpr int kRowsWave = 32;
+constexpr int kRowsWave = kMfmaRowsPerWave;
 constexpr int kKT = 128;       // keys per LDS tile (four 32-key blocks)
 constexpr int kPadK = 8;       // K row padding (bf16): 16-byte reads conflict-free
 constexpr int kPadV = 16;      // V row padding (bf16): transpose reads conflict-free
 constexpr int kPadO = 8;       // output staging row padding (bf16)
-static_assert(kWaves * kRowsWave == kMfmaRowsPerTile, "tile rows");
 
 template <int D>
 struct Smem {
@@ -125,25 +124,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   Smem<D>& sm = *reinterpret_cast<Smem<D>*>(smem_raw);
 
-  // XCD-aware mapping: consecutive workgroup ids go round-robin over the 8 XCDs;
-  // give each XCD a contiguous range of (layer, KV head, row tile) work items.
-  const int n_work = a.n_layers * a.H_kv * a.n_qtiles;
-  const int per_xcd = gridDim.x >> 3;
-  const int wid = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (wid >= n_work) return;
-  const int qt = wid % a.n_qtiles;
-  const int lg = wid / a.n_qtiles;
+  // The host plan fixes each workgroup's (layer, KV head), row range and
+  // row-tile slot; it already places the work of one (layer, KV head) on one XCD.
+  const AttnWork wk = a.work[blockIdx.x];
+  if (wk.rows <= 0) return;
+  const int lg = wk.lg;
   const int layer = lg / a.H_kv, g = lg % a.H_kv;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, h = lane >> 5;
-  const int GT = a.G * a.T;
   const int S = a.S, n_keys = a.S + a.T;
   const int n_tiles = (n_keys + kKT - 1) / kKT;
   const int first_masked = S / kKT;  // tiles from here on contain frame keys or the ragged end
-  const int row0 = qt * kMfmaRowsPerTile + wave * kRowsWave;
-  const bool active = row0 < GT;
+  const int row_end = wk.row0 + wk.rows;  // rows of this workgroup: [wk.row0, row_end)
+  const int row0 = wk.row0 + wave * kRowsWave;
+  const bool active = row0 < row_end;
   const float c = a.scale_log2;
 
   const uint16_t* qg = static_cast<const uint16_t*>(a.q) + static_cast<size_t>(layer * a.H_q + g * a.G) * a.T * D;
@@ -151,11 +147,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const uint16_t* vst = static_cast<const uint16_t*>(a.vs) + static_cast<size_t>(lg) * a.B * D;
   const uint16_t* kfr = static_cast<const uint16_t*>(a.kf) + static_cast<size_t>(lg) * a.T * D;
   const uint16_t* vfr = static_cast<const uint16_t*>(a.vf) + static_cast<size_t>(lg) * a.T * D;
-  float* part = a.partial + (static_cast<size_t>(lg) * a.n_qtiles + qt) * a.pool_stride;
+  float* part = a.partial + (static_cast<size_t>(lg) * a.tile_stride + wk.tile) * a.pool_stride;
 
   // Q^T operand (B of K Q^T) in registers; an invalid row is zero and sees no key.
   const int r_lane = row0 + l32;
-  const bool row_valid = r_lane < GT;
+  const bool row_valid = r_lane < row_end;
   const int lim = row_valid ? S + (r_lane % a.T) : -1;  // candidate j is visible iff j <= lim
   bf16x8 qreg[KS];
 #pragma unroll
@@ -365,7 +361,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     for (int it = 0; it < kRowsWave * KCH / 64; ++it) {
       const int idx = it * 64 + lane;
       const int r = idx / KCH, ch = idx % KCH;
-      if (row0 + r < GT)
+      if (row0 + r < row_end)
         *reinterpret_cast<u32x4*>(og + static_cast<size_t>(row0 + r) * D + ch * 8) =
             *reinterpret_cast<const u32x4*>(ost + r * (D + kPadO) + ch * 8);
     }
@@ -373,8 +369,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
 }
 
 hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
-  const int n_work = a.n_layers * a.H_kv * a.n_qtiles;
-  const int grid = ((n_work + 7) / 8) * 8;
+  const int grid = a.n_work;
   if (head_dim == 128) {
     hipLaunchKernelGGL(attn_mfma_kernel<128>, dim3(grid), dim3(kThreads), sizeof(Smem<128>), s, a);
   } else {

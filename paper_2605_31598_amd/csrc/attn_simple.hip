@@ -60,7 +60,7 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
   const T* vst = static_cast<const T*>(a.vs) + static_cast<size_t>(lg) * a.B * D;
   const T* kfr = static_cast<const T*>(a.kf) + static_cast<size_t>(lg) * a.T * D;
   const T* vfr = static_cast<const T*>(a.vf) + static_cast<size_t>(lg) * a.T * D;
-  float* part = a.partial + (static_cast<size_t>(lg) * a.n_qtiles + qt) * a.pool_stride;
+  float* part = a.partial + (static_cast<size_t>(lg) * a.tile_stride + qt) * a.pool_stride;
 
   float q[D];
   for (int e = 0; e < D; ++e) q[e] = valid ? load_elem(qrow + e) : 0.f;
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
 }
 
 hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s) {
-  dim3 grid(a.n_qtiles, a.n_layers * a.H_kv);
+  dim3 grid((a.G * a.T + kSimpleRowsPerTile - 1) / kSimpleRowsPerTile, a.n_layers * a.H_kv);
   dim3 block(64);
   if (bf16) {
     if (head_dim == 64) hipLaunchKernelGGL((attn_simple_kernel<uint16_t, 64>), grid, block, 0, s, a);

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "plan.h"
+
 namespace skv {
 
 // One attention launch covers `n_layers` consecutive layers of one frame.
@@ -16,9 +18,11 @@ struct AttnArgs {
   const void* ks;      // [n_layers][H_kv][B][d]   state keys (slots 0..S-1 valid)
   const void* vs;      // [n_layers][H_kv][B][d]   state values
   void* out;           // [n_layers][H_q][T][d]
-  float* partial;      // [n_layers][H_kv][n_qtiles][pool_stride] column sums of P per row tile
+  float* partial;      // [n_layers][H_kv][tile_stride][pool_stride] column sums of P per row tile
+  const AttnWork* work;  // MFMA kernel: one work item per workgroup (n_work of them)
+  int n_work;
   int n_layers, H_q, H_kv, G, T, B, S;
-  int n_qtiles, pool_stride;
+  int tile_stride, pool_stride;
   float scale_log2;    // softmax scale * log2(e)
 };
 
@@ -27,7 +31,8 @@ struct AttnArgs {
 // decode-cache append in a second set of workgroups of the same grid.
 struct RefreshArgs {
   const float* partial;      // as in AttnArgs
-  int n_qtiles, pool_stride;
+  const int32_t* lg_tiles;   // [n_layers][H_kv] row tiles the attention launch wrote
+  int tile_stride, pool_stride;
   const void* kf;            // [n_layers][H_kv][T][d]   frame keys
   const void* vf;            //                          frame values
   void* ks;                  // [n_layers][H_kv][B][d]   state slots
@@ -47,7 +52,8 @@ struct RefreshArgs {
   float inv_T;
 };
 
-constexpr int kMfmaRowsPerTile = 256;   // query rows (G*T packed) per attention workgroup
+constexpr int kMfmaRowsPerWave = 32;    // query rows (G*T packed) per attention wave
+constexpr int kMfmaWaves = 8;           // waves per attention workgroup (at most)
 constexpr int kSimpleRowsPerTile = 64;
 constexpr int kSelectThreads = 1024;
 constexpr int kMaxPool = 16384;         // B + T limit (selection keeps the pool in LDS)

@@ -172,7 +172,8 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
   const int S = a.S, T = a.T, B = a.B, P = S + T;
   uint32_t* sbits = pool_mem;
   int32_t* spos = reinterpret_cast<int32_t*>(pool_mem + P);
-  const float* part = a.partial + static_cast<size_t>(lg) * a.n_qtiles * a.pool_stride;
+  const float* part = a.partial + static_cast<size_t>(lg) * a.tile_stride * a.pool_stride;
+  const int n_tiles = a.lg_tiles[lg];
   int32_t* state_pos = a.state_pos + static_cast<size_t>(lg) * B;
   float* sscore = a.state_score + static_cast<size_t>(lg) * B;
   float* pscore = a.pool_score + static_cast<size_t>(lg) * a.pool_stride;
@@ -182,7 +183,7 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
 
   for (int j = tid; j < P; j += blockDim.x) {
     float acc = 0.f;
-    for (int t = 0; t < a.n_qtiles; ++t) acc += part[static_cast<size_t>(t) * a.pool_stride + j];
+    for (int t = 0; t < n_tiles; ++t) acc += part[static_cast<size_t>(t) * a.pool_stride + j];
     const float s = acc * a.inv_T;
     const int32_t pos = j < S ? state_pos[j] : a.frame_pos0 + (j - S);
     pscore[j] = s;

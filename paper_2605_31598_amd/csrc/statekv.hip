@@ -50,7 +50,7 @@ struct skv_ctx {
   int G = 1;
   float scale_log2 = 0.f;
   bool use_mfma = false;
-  int n_qtiles = 0;
+  int tile_stride = 0;  // row-tile slots per (layer, KV head) in `partial`
   int pool_stride = 0;
   size_t row_bytes = 0;
   int64_t max_tokens = 0;
@@ -62,11 +62,19 @@ struct skv_ctx {
   float* state_score = nullptr;
   void* cache_k = nullptr;   // [L][H_kv][max_tokens][d]
   void* cache_v = nullptr;
-  float* partial = nullptr;  // [L][H_kv][n_qtiles][pool_stride]
+  float* partial = nullptr;  // [L][H_kv][tile_stride][pool_stride]
   float* pool_score = nullptr;     // [L][H_kv][pool_stride]
   int32_t* pool_pos = nullptr;
   int32_t* admit_src = nullptr;    // [L][H_kv][T]
   int32_t* admit_dst = nullptr;
+  // attention work plans, one per layer_count (index layer_count - 1), in one
+  // device allocation; the fp32 path uses fixed 64-row tiles instead
+  struct Plan {
+    const skv::AttnWork* work = nullptr;
+    const int32_t* tiles = nullptr;  // row tiles per (layer, KV head) of the call
+    int n_work = 0;
+  };
+  std::vector<Plan> plans;
   std::vector<void*> allocations;
 
   // progress of the stream
@@ -107,6 +115,53 @@ int layer_frames_done(const skv_ctx* c, int layer) {
 int state_size(const skv_ctx* c, int64_t frames_done) {
   const int64_t seen = frames_done * c->cfg.tokens_per_frame;
   return static_cast<int>(seen < c->cfg.capacity ? seen : c->cfg.capacity);
+}
+
+// Uploads the attention work plan of every layer_count (1 .. n_layers).  The
+// plans depend only on the shape and the device's compute-unit count.
+skv_status build_plans(skv_ctx* c, int rows) {
+  const skv_config& cfg = c->cfg;
+  std::vector<skv::AttnPlan> host(static_cast<size_t>(cfg.n_layers));
+  if (c->use_mfma) {
+    int cu = 0;
+    const hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, c->device);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    const int n_xcd = (cu >= 8 && cu % 8 == 0) ? 8 : 1;  // workgroups go round-robin over the XCDs
+    for (int lc = 1; lc <= cfg.n_layers; ++lc)
+      host[static_cast<size_t>(lc - 1)] = skv::plan_attention(lc * cfg.n_kv_heads, rows, skv::kMfmaRowsPerWave,
+                                                               skv::kMfmaWaves, n_xcd, cu / n_xcd);
+  } else {
+    // fp32 path: every (layer, KV head) writes ceil(rows / 64) tiles; one
+    // table of the largest call serves all calls
+    host[static_cast<size_t>(cfg.n_layers - 1)].tiles.assign(static_cast<size_t>(cfg.n_layers) * cfg.n_kv_heads,
+                                                              c->tile_stride);
+  }
+  size_t bytes = 0;
+  for (const auto& p : host) bytes += p.items.size() * sizeof(skv::AttnWork) + p.tiles.size() * sizeof(int32_t);
+  std::vector<char> blob(bytes);
+  void* dev = nullptr;
+  skv_status s = alloc(c, bytes, &dev);
+  if (s != SKV_OK) return s;
+  c->plans.assign(static_cast<size_t>(cfg.n_layers), skv_ctx::Plan{});
+  size_t off = 0;
+  for (size_t i = 0; i < host.size(); ++i) {
+    const auto& p = host[i];
+    skv_ctx::Plan& d = c->plans[i];
+    d.work = reinterpret_cast<const skv::AttnWork*>(static_cast<char*>(dev) + off);
+    d.n_work = static_cast<int>(p.items.size());
+    if (!p.items.empty()) std::memcpy(blob.data() + off, p.items.data(), p.items.size() * sizeof(skv::AttnWork));
+    off += p.items.size() * sizeof(skv::AttnWork);
+    d.tiles = reinterpret_cast<const int32_t*>(static_cast<char*>(dev) + off);
+    if (!p.tiles.empty()) std::memcpy(blob.data() + off, p.tiles.data(), p.tiles.size() * sizeof(int32_t));
+    off += p.tiles.size() * sizeof(int32_t);
+  }
+  if (!c->use_mfma)
+    for (auto& d : c->plans) d.tiles = c->plans.back().tiles;
+  if (bytes > 0) {
+    const hipError_t e = hipMemcpy(dev, blob.data(), bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy of the attention plans");
+  }
+  return SKV_OK;
 }
 
 }  // namespace
@@ -158,8 +213,8 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   ctx->scale_log2 = scale * 1.4426950408889634f;
   const char* force_simple = std::getenv("SKV_FORCE_SIMPLE_ATTENTION");
   ctx->use_mfma = c.dtype == SKV_BF16 && !(force_simple && force_simple[0] == '1');
-  const int rows_per_tile = ctx->use_mfma ? skv::kMfmaRowsPerTile : skv::kSimpleRowsPerTile;
-  ctx->n_qtiles = static_cast<int>((rows + rows_per_tile - 1) / rows_per_tile);
+  ctx->tile_stride = ctx->use_mfma ? skv::plan_max_tiles(static_cast<int>(rows), skv::kMfmaRowsPerWave, skv::kMfmaWaves)
+                                  : static_cast<int>((rows + skv::kSimpleRowsPerTile - 1) / skv::kSimpleRowsPerTile);
   ctx->pool_stride = ((c.capacity + c.tokens_per_frame + 63) / 64) * 64;
   ctx->row_bytes = static_cast<size_t>(c.head_dim) * ctx->elem;
   ctx->max_tokens = max_tokens;
@@ -187,7 +242,7 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
       {reinterpret_cast<void**>(&ctx->state_score), LH * c.capacity * sizeof(float)},
       {&ctx->cache_k, cache_bytes},
       {&ctx->cache_v, cache_bytes},
-      {reinterpret_cast<void**>(&ctx->partial), LH * ctx->n_qtiles * ctx->pool_stride * sizeof(float)},
+      {reinterpret_cast<void**>(&ctx->partial), LH * ctx->tile_stride * ctx->pool_stride * sizeof(float)},
       {reinterpret_cast<void**>(&ctx->pool_score), LH * ctx->pool_stride * sizeof(float)},
       {reinterpret_cast<void**>(&ctx->pool_pos), LH * ctx->pool_stride * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_src), LH * c.tokens_per_frame * sizeof(int32_t)},
@@ -206,6 +261,12 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
       delete ctx;
       return hip_fail(e, "hipMemsetAsync");
     }
+  }
+  const skv_status ps = build_plans(ctx, static_cast<int>(rows));
+  if (ps != SKV_OK) {
+    release(ctx);
+    delete ctx;
+    return ps;
   }
   *out = ctx;
   return SKV_OK;
@@ -240,7 +301,10 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.ks = static_cast<char*>(ctx->state_k) + lh0 * B * rb;
   aa.vs = static_cast<char*>(ctx->state_v) + lh0 * B * rb;
   aa.out = out;
-  aa.partial = ctx->partial + lh0 * ctx->n_qtiles * ctx->pool_stride;
+  const skv_ctx::Plan& plan = ctx->plans[static_cast<size_t>(layer_count - 1)];
+  aa.partial = ctx->partial + lh0 * ctx->tile_stride * ctx->pool_stride;
+  aa.work = plan.work;
+  aa.n_work = plan.n_work;
   aa.n_layers = layer_count;
   aa.H_q = c.n_q_heads;
   aa.H_kv = Hkv;
@@ -248,13 +312,14 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.T = T;
   aa.B = B;
   aa.S = S;
-  aa.n_qtiles = ctx->n_qtiles;
+  aa.tile_stride = ctx->tile_stride;
   aa.pool_stride = ctx->pool_stride;
   aa.scale_log2 = ctx->scale_log2;
 
   skv::RefreshArgs ra;
   ra.partial = aa.partial;
-  ra.n_qtiles = ctx->n_qtiles;
+  ra.lg_tiles = plan.tiles;
+  ra.tile_stride = ctx->tile_stride;
   ra.pool_stride = ctx->pool_stride;
   ra.kf = k;
   ra.vf = v;

@@ -1,0 +1,113 @@
+"""Host checks of the attention work planner (paper_2605_31598_amd/csrc/plan.cpp).
+
+The planner decides which query rows of which (layer, KV head) each attention
+workgroup covers; a mistake there would make the kernel skip or repeat rows.
+It is plain C++, so it is compiled here with g++ and run on the CPU:
+
+* every query row of every (layer, KV head) is covered exactly once, by whole
+  32-row waves, at most 8 waves per workgroup;
+* row-tile slots of one (layer, KV head) are 0 .. tiles-1, each used once, and
+  never more than plan_max_tiles (the size of the column-sum buffer);
+* all work of one (layer, KV head) lands on one XCD (workgroup i runs on XCD i % 8);
+* on each XCD the full workgroups come before the short ones;
+* for the 7B-shaped 28-layer stack on 256 compute units the full workgroups fill
+  exactly two rounds and the rest fits one round of <= 4-wave workgroups.
+"""
+import os
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2605_31598_amd", "csrc")
+
+DRIVER = r'''
+#include <cstdio>
+#include <cstdlib>
+#include "plan.h"
+int main(int argc, char** argv) {
+  const int n_lg = atoi(argv[1]), rows = atoi(argv[2]), n_xcd = atoi(argv[3]), cu = atoi(argv[4]);
+  const skv::AttnPlan p = skv::plan_attention(n_lg, rows, 32, 8, n_xcd, cu);
+  printf("bound %d\n", skv::plan_max_tiles(rows, 32, 8));
+  for (size_t i = 0; i < p.tiles.size(); ++i) printf("tiles %zu %d\n", i, p.tiles[i]);
+  for (const auto& w : p.items) printf("item %d %d %d %d\n", w.lg, w.row0, w.rows, w.tile);
+  return 0;
+}
+'''
+
+
+@pytest.fixture(scope="module")
+def planner(tmp_path_factory):
+    d = tmp_path_factory.mktemp("plan")
+    src = d / "driver.cpp"
+    src.write_text(DRIVER)
+    exe = d / "driver"
+    subprocess.run(["g++", "-O1", "-std=c++17", "-I", CSRC, str(src), os.path.join(CSRC, "plan.cpp"), "-o", str(exe)],
+                   check=True)
+
+    def run(n_lg, rows, n_xcd=8, cu_per_xcd=32):
+        out = subprocess.run([str(exe), str(n_lg), str(rows), str(n_xcd), str(cu_per_xcd)], capture_output=True,
+                             text=True, check=True).stdout.split("\n")
+        bound = int(out[0].split()[1])
+        tiles = [int(l.split()[2]) for l in out if l.startswith("tiles")]
+        items = [tuple(int(x) for x in l.split()[1:]) for l in out if l.startswith("item")]
+        return bound, tiles, items
+
+    return run
+
+
+SHAPES = [(112, 1372), (4, 1372), (640, 2048), (8, 2916), (2, 32), (28, 1372), (4, 196), (1, 37), (3, 1),
+          (7, 7 * 196), (80, 2048 + 5), (13, 300), (9, 8 * 32 * 3 + 1)]
+
+
+@pytest.mark.parametrize("n_lg,rows", SHAPES)
+@pytest.mark.parametrize("n_xcd,cu", [(8, 32), (1, 4), (8, 1)])
+def test_plan_covers_every_row_once(planner, n_lg, rows, n_xcd, cu):
+    bound, tiles, items = planner(n_lg, rows, n_xcd, cu)
+    assert len(tiles) == n_lg
+    covered = [[] for _ in range(n_lg)]
+    slots = [set() for _ in range(n_lg)]
+    xcd_of = {}
+    for i, (lg, row0, nrows, tile) in enumerate(items):
+        if nrows == 0:
+            continue
+        assert 0 <= lg < n_lg
+        assert row0 % 32 == 0 and 0 < nrows <= 8 * 32 and row0 + nrows <= rows
+        assert nrows % 32 == 0 or row0 + nrows == rows  # only the last wave of a range is ragged
+        covered[lg].append((row0, row0 + nrows))
+        assert tile not in slots[lg]
+        slots[lg].add(tile)
+        assert xcd_of.setdefault(lg, i % n_xcd) == i % n_xcd, "one (layer, KV head) split over XCDs"
+    for lg in range(n_lg):
+        spans = sorted(covered[lg])
+        assert spans[0][0] == 0 and spans[-1][1] == rows
+        assert all(a[1] == b[0] for a, b in zip(spans, spans[1:])), f"gap or overlap in range {lg}"
+        assert slots[lg] == set(range(tiles[lg]))
+        assert tiles[lg] <= bound
+
+
+@pytest.mark.parametrize("n_lg,rows", SHAPES)
+def test_full_workgroups_first_on_each_xcd(planner, n_lg, rows):
+    _, _, items = planner(n_lg, rows)
+    for x in range(8):
+        seq = [it for it in items[x::8] if it[2] > 0]
+        full = [it[2] == 256 for it in seq]
+        assert full == sorted(full, reverse=True)
+
+
+def test_7b_stack_two_full_rounds_then_short_round(planner):
+    _, tiles, items = planner(28 * 4, 7 * 196)
+    real = [it for it in items if it[2] > 0]
+    full = [it for it in real if it[2] == 256]
+    short = [it for it in real if it[2] < 256]
+    assert len(full) == 2 * 256
+    assert len(short) <= 256 and all(it[2] <= 4 * 32 for it in short)
+    assert max(tiles) <= 7
+
+
+def test_small_call_uses_short_workgroups(planner):
+    # one layer of the 7B shape: 43 wave blocks per KV head fit one round of <= 4-wave workgroups
+    _, tiles, items = planner(4, 7 * 196)
+    real = [it for it in items if it[2] > 0]
+    assert all(it[2] <= 128 for it in real)
+    assert tiles == [11] * 4
