@@ -26,6 +26,12 @@ What one frame step computes, per layer and per KV head, in the paper's order
    D (never read during prefill), and the virtual length L_n grows by T;
    token positions come from L_n (virtual sequence length paragraph).
 
+Two baselines of the evaluation share these steps and differ only in which
+candidates survive step 4: the recency window (keep the B most recent
+candidates, ReKV-style: the last B / T frames when T divides B) and streaming
+full self-attention (Full SA: keep every candidate, so frame n attends to all
+earlier tokens).
+
 All arithmetic is fp64 NumPy.  Inputs are the exact bf16/fp32 values widened
 to fp64.  Readings of points the paper leaves open are listed in the design
 notes shipped with the repository and restated at each function below.
@@ -144,11 +150,31 @@ def select_top(scores, pos, capacity):
     return keep[np.argsort(pos[keep], kind="stable")]
 
 
-def frame_step(state: LayerState, q, k, v, frame, capacity, scale=None, pos_offset=0,
-               keep_attn=False) -> StepResult:
-    """One layer of one frame: attention over [C_{n-1}; frame], scores, Top-B refresh.
+def select_recent(pos, capacity):
+    """Recency-window baseline: indices of the ``capacity`` largest positions (positions
+    are distinct, so there are no ties); everything when the pool fits.  Ascending in
+    position."""
+    P = pos.shape[0]
+    if P <= capacity:
+        keep = np.arange(P)
+    else:
+        keep = np.argsort(-pos, kind="stable")[:capacity]
+    return keep[np.argsort(pos[keep], kind="stable")]
 
-    q [H_q, T, d], k/v [H_kv, T, d] as float64 (exact widened input values)."""
+
+POLICIES = ("statekv", "recent", "full")
+
+
+def frame_step(state: LayerState, q, k, v, frame, capacity, scale=None, pos_offset=0,
+               keep_attn=False, policy="statekv") -> StepResult:
+    """One layer of one frame: attention over [C_{n-1}; frame], scores, refresh.
+
+    q [H_q, T, d], k/v [H_kv, T, d] as float64 (exact widened input values).
+    ``policy`` picks the refresh: "statekv" (Top-B by score, Eq. 6), "recent" (the B
+    most recent candidates) or "full" (keep every candidate; ``capacity`` ignored, so
+    the state is the whole token history and the step is streaming full attention)."""
+    if policy not in POLICIES:
+        raise ValueError(f"unknown policy {policy!r}")
     H_q, T, d = q.shape
     H_kv = k.shape[0]
     if scale is None:
@@ -171,10 +197,15 @@ def frame_step(state: LayerState, q, k, v, frame, capacity, scale=None, pos_offs
         if keep_attn:
             attn[hs] = a_g
 
+    if policy == "full":
+        capacity = S + T
     n_keep = min(capacity, S + T)
     kept = np.empty((H_kv, n_keep), dtype=np.int64)
     for g in range(H_kv):
-        kept[g] = select_top(scores[g], pool_pos[g], capacity)
+        if policy == "recent":
+            kept[g] = select_recent(pool_pos[g], capacity)
+        else:
+            kept[g] = select_top(scores[g], pool_pos[g], capacity)
     rows = np.arange(H_kv)[:, None]
     new_state = LayerState(
         pos=pool_pos[rows, kept].copy(),
@@ -206,7 +237,7 @@ class DecodeCache:
 
 
 def run_layer(inputs, n_frames, capacity, n_kv_heads, head_dim, scale=None, pos_offset=0,
-              state=None, start_frame=0, callback=None):
+              state=None, start_frame=0, callback=None, policy="statekv"):
     """Stream ``n_frames`` frames of one layer.  ``inputs(frame)`` returns float64
     (q, k, v).  Returns (final state, decode cache, list of StepResult)."""
     st = state.copy() if state is not None else LayerState.empty(n_kv_heads, head_dim)
@@ -214,7 +245,7 @@ def run_layer(inputs, n_frames, capacity, n_kv_heads, head_dim, scale=None, pos_
     results = []
     for n in range(start_frame, start_frame + n_frames):
         q, k, v = inputs(n)
-        r = frame_step(st, q, k, v, n, capacity, scale, pos_offset)
+        r = frame_step(st, q, k, v, n, capacity, scale, pos_offset, policy=policy)
         cache.append(k, v)  # D_n = D_{n-1} with the frame's K/V appended
         st = r.state
         results.append(r if callback is None else callback(n, r))

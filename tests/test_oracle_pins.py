@@ -126,6 +126,48 @@ def check_zero_capacity_is_framewise_sdpa(seed=2, H_q=4, H_kv=2, d=8, T=6, N=3):
         assert r.state.size == 0
 
 
+def check_full_policy_is_causal_sdpa(seed=5, H_q=6, H_kv=3, d=8, T=4, N=5, B=3):
+    """Full SA: whatever the capacity, frame n attends to every earlier token, so the
+    outputs of the stream are one causal attention over all N*T tokens."""
+    video = random_video(seed, H_q, H_kv, d, T, N)
+    scale = d ** -0.5
+    st = orc.LayerState.empty(H_kv, d)
+    q = np.concatenate([x[0] for x in video], axis=1)
+    k = np.concatenate([x[1] for x in video], axis=1)
+    v = np.concatenate([x[2] for x in video], axis=1)
+    o_full = sdpa_causal(q, k, v, scale)
+    for n, (qn, kn, vn) in enumerate(video):
+        r = orc.frame_step(st, qn, kn, vn, n, B, scale, policy="full")
+        np.testing.assert_allclose(r.out, o_full[:, n * T:(n + 1) * T], rtol=0, atol=1e-12)
+        assert np.array_equal(r.state.pos, np.tile(np.arange((n + 1) * T), (H_kv, 1)))
+        st = r.state
+
+
+def check_recent_policy_window(seed=6, H_q=4, H_kv=2, d=8, T=5, N=6, B=7, pos_offset=3):
+    """Recency window: the state entering frame n is the last min(B, n*T) tokens, and the
+    frame attends to exactly those (fully visible) plus itself (causal)."""
+    video = random_video(seed, H_q, H_kv, d, T, N)
+    scale = d ** -0.5
+    st = orc.LayerState.empty(H_kv, d)
+    ks = np.concatenate([x[1] for x in video], axis=1)
+    vs = np.concatenate([x[2] for x in video], axis=1)
+    G = H_q // H_kv
+    for n, (qn, kn, vn) in enumerate(video):
+        S = min(B, n * T)
+        np.testing.assert_array_equal(st.pos, np.tile(pos_offset + np.arange(n * T - S, n * T), (H_kv, 1)))
+        r = orc.frame_step(st, qn, kn, vn, n, B, scale, pos_offset, policy="recent")
+        keys = slice(n * T - S, (n + 1) * T)
+        allow = np.zeros((T, S + T), dtype=bool)
+        for i in range(T):
+            allow[i, :S + i + 1] = True
+        o = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(qn)[None], torch.from_numpy(ks[:, keys]).repeat_interleave(G, dim=0)[None],
+            torch.from_numpy(vs[:, keys]).repeat_interleave(G, dim=0)[None],
+            attn_mask=torch.from_numpy(allow), scale=scale)[0].numpy()
+        np.testing.assert_allclose(r.out, o, rtol=0, atol=1e-12)
+        st = r.state
+
+
 def check_zero_query_closed_form(H_q=6, H_kv=3, d=4, T=5, N=6, B=7):
     G = H_q // H_kv
     rng = np.random.default_rng(3)
@@ -163,6 +205,15 @@ def check_bruteforce(seed, H_q, H_kv, d, T, B, N, pos_offset):
 # ----------------------------------------------------------------------------
 # tests
 # ----------------------------------------------------------------------------
+def test_full_policy_equals_causal_sdpa_over_the_stream():
+    check_full_policy_is_causal_sdpa()
+
+
+def test_recent_policy_keeps_the_last_tokens():
+    check_recent_policy_window()
+    check_recent_policy_window(seed=7, T=4, B=8, N=5, pos_offset=0)  # window of whole frames
+
+
 def test_golden_handworked():
     check_golden()
 
@@ -345,10 +396,17 @@ def _mut_positions_physical(frame, T, pos_offset=0):
     return pos_offset + np.arange(T, dtype=np.int64) + frame  # wrong: not from the virtual length
 
 
+def _mut_recent_oldest(pos, capacity):
+    P = pos.shape[0]
+    keep = np.arange(P) if P <= capacity else np.argsort(pos, kind="stable")[:capacity]  # wrong: oldest
+    return keep[np.argsort(pos[keep], kind="stable")]
+
+
 PINS = [check_golden, check_full_capacity_is_causal_sdpa,
         lambda: check_full_capacity_is_causal_sdpa(seed=11, H_q=14, H_kv=2, d=16, T=7, N=3),
         check_zero_capacity_is_framewise_sdpa, check_zero_query_closed_form,
-        lambda: check_bruteforce(1, 4, 2, 4, 4, 3, 4, 5)]
+        lambda: check_bruteforce(1, 4, 2, 4, 4, 3, 4, 5), check_full_policy_is_causal_sdpa,
+        check_recent_policy_window]
 
 
 @pytest.mark.parametrize("name,attr,mutant", [
@@ -360,6 +418,7 @@ PINS = [check_golden, check_full_capacity_is_causal_sdpa,
     ("ties to higher position", "select_top", _mut_select_high_pos),
     ("keeps the lowest scores", "select_top", _mut_select_lowest),
     ("positions from physical length", "frame_positions", _mut_positions_physical),
+    ("recency window keeps the oldest", "select_recent", _mut_recent_oldest),
 ])
 def test_planted_mistake_is_caught(monkeypatch, name, attr, mutant):
     monkeypatch.setattr(orc, attr, mutant)
