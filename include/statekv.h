@@ -47,6 +47,22 @@ typedef enum {
 
 typedef enum { SKV_BF16 = 0, SKV_F32 = 1 } skv_dtype;
 
+/* What the cross-frame context of a layer is (selection paragraph of the
+ * method, and the two baselines of the evaluation):
+ *   SKV_POLICY_STATEKV  the compressed state C_n: the B candidates of state and
+ *                       frame with the highest importance score (Eq. 6), ties
+ *                       to the lowest position;
+ *   SKV_POLICY_RECENT   the B most recent tokens (the recency-window baseline,
+ *                       ReKV-style: a window of the last B / T frames when T
+ *                       divides B); importance scores are still computed and
+ *                       reported, but do not decide;
+ *   SKV_POLICY_FULL     no compression: frame n attends to every earlier token,
+ *                       read from the decode cache D (streaming full
+ *                       self-attention, the Full SA baseline); capacity is
+ *                       ignored, no scores are computed and the state stays
+ *                       empty. */
+typedef enum { SKV_POLICY_STATEKV = 0, SKV_POLICY_RECENT = 1, SKV_POLICY_FULL = 2 } skv_policy;
+
 /* Problem statement of the method: head counts and head dimension d_h (Eq. 5),
  * T tokens per frame, capacity B of the compressed state (Eq. 4), layer count,
  * and the decode-cache length, which grows by T per frame. */
@@ -61,6 +77,8 @@ typedef struct {
   int32_t dtype;            /* skv_dtype of Q, K, V, the output and both caches */
   float softmax_scale;      /* logit scale; 0 selects 1/sqrt(head_dim) */
   int64_t pos_offset;       /* virtual position of the first video token (room for a text prefix) */
+  int32_t policy;           /* skv_policy; 0 (a zeroed config) is StateKV */
+  int32_t reserved;         /* must be 0 */
 } skv_config;
 
 typedef struct skv_ctx skv_ctx;
@@ -68,14 +86,17 @@ typedef struct skv_ctx skv_ctx;
 /* Validates cfg, allocates and zeroes every device buffer of one video stream
  * (compressed state and decode cache of all layers, scratch), and binds the
  * context to hip_stream (a hipStream_t; NULL means the default stream).
- * Limits: pos_offset + max_frames * T < 2^31; B + T <= 16384.
+ * Limits: pos_offset + max_frames * T < 2^31; B + T <= 16384 (STATEKV and
+ * RECENT); policy one of skv_policy and reserved = 0, else SKV_ERR_INVALID_ARG.
  * Returns SKV_OK and *out, or an error and *out = NULL. */
 skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
 
 /* Runs layers [layer_begin, layer_begin + layer_count) of the current frame n:
  * attention with fused importance scoring (Eq. 5 and the score), Top-B refresh
  * of each layer's compressed state (Eq. 6), and append of the frame's K/V to
- * each layer's decode cache.  Layers of one frame must be stepped in order;
+ * each layer's decode cache.  Under SKV_POLICY_RECENT the refresh keeps the B
+ * most recent candidates; under SKV_POLICY_FULL the frame attends to all
+ * n * T cached tokens plus itself (causal), and only the append follows.  Layers of one frame must be stepped in order;
  * the frame counter advances after the last layer.  layer_count = n_layers
  * runs the whole stack in one launch per stage.
  * Device layouts (row-major, dtype of the config):

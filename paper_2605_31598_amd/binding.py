@@ -25,6 +25,11 @@ SKV_ERR_UNSUPPORTED = -6
 
 SKV_BF16 = 0
 SKV_F32 = 1
+
+SKV_POLICY_STATEKV = 0
+SKV_POLICY_RECENT = 1
+SKV_POLICY_FULL = 2
+POLICIES = {"statekv": SKV_POLICY_STATEKV, "recent": SKV_POLICY_RECENT, "full": SKV_POLICY_FULL}
 N_STAGES = 2
 STAGES = ("attention", "refresh")
 
@@ -40,7 +45,7 @@ class skv_config(ctypes.Structure):
         ("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
         ("head_dim", ctypes.c_int32), ("tokens_per_frame", ctypes.c_int32), ("capacity", ctypes.c_int32),
         ("max_frames", ctypes.c_int32), ("dtype", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
-        ("pos_offset", ctypes.c_int64),
+        ("pos_offset", ctypes.c_int64), ("policy", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
 

@@ -56,11 +56,12 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
 
   const T* qrow = static_cast<const T*>(a.q) +
                   (static_cast<size_t>(layer * a.H_q + g * a.G) * a.T + (valid ? r : 0)) * D;
-  const T* kst = static_cast<const T*>(a.ks) + static_cast<size_t>(lg) * a.B * D;
-  const T* vst = static_cast<const T*>(a.vs) + static_cast<size_t>(lg) * a.B * D;
+  const T* kst = static_cast<const T*>(a.ks) + static_cast<size_t>(lg) * a.kv_rows * D;
+  const T* vst = static_cast<const T*>(a.vs) + static_cast<size_t>(lg) * a.kv_rows * D;
   const T* kfr = static_cast<const T*>(a.kf) + static_cast<size_t>(lg) * a.T * D;
   const T* vfr = static_cast<const T*>(a.vf) + static_cast<size_t>(lg) * a.T * D;
-  float* part = a.partial + (static_cast<size_t>(lg) * a.tile_stride + qt) * a.pool_stride;
+  // no partial buffer: streaming full attention, which computes no scores
+  float* part = a.partial ? a.partial + (static_cast<size_t>(lg) * a.tile_stride + qt) * a.pool_stride : nullptr;
 
   float q[D];
   for (int e = 0; e < D; ++e) q[e] = valid ? load_elem(qrow + e) : 0.f;
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
       ps[tid][kk] = p;
     }
     __syncthreads();
-    if (tid < KT && t0 + tid < n_keys) {
+    if (part && tid < KT && t0 + tid < n_keys) {
       float c = 0.f;
       for (int rr = 0; rr < kSimpleRowsPerTile; ++rr) c += ps[rr][tid];
       part[t0 + tid] = c;

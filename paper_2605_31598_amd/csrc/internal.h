@@ -15,13 +15,15 @@ struct AttnArgs {
   const void* q;       // [n_layers][H_q][T][d]
   const void* kf;      // [n_layers][H_kv][T][d]   frame keys
   const void* vf;      // [n_layers][H_kv][T][d]   frame values
-  const void* ks;      // [n_layers][H_kv][B][d]   state keys (slots 0..S-1 valid)
-  const void* vs;      // [n_layers][H_kv][B][d]   state values
+  const void* ks;      // [n_layers][H_kv][kv_rows][d]  earlier keys, rows 0..S-1 valid: the
+  const void* vs;      //   compressed state (kv_rows = B) or the decode cache (kv_rows = max_tokens)
   void* out;           // [n_layers][H_q][T][d]
-  float* partial;      // [n_layers][H_kv][tile_stride][pool_stride] column sums of P per row tile
+  float* partial;      // [n_layers][H_kv][tile_stride][pool_stride] column sums of P per row
+                       // tile; null for streaming full attention (no scores)
   const AttnWork* work;  // MFMA kernel: one work item per workgroup (n_work of them)
   int n_work;
   int n_layers, H_q, H_kv, G, T, B, S;
+  int kv_rows;
   int tile_stride, pool_stride;
   float scale_log2;    // softmax scale * log2(e)
 };
@@ -50,6 +52,7 @@ struct RefreshArgs {
   int row_bytes;             // d * element size, a multiple of 16
   int32_t frame_pos0;        // virtual position of frame token 0
   float inv_T;
+  int mode;                  // 0: Top-B by score, 1: the B most recent, 2: append only
 };
 
 constexpr int kMfmaRowsPerWave = 32;    // query rows (G*T packed) per attention wave
@@ -59,6 +62,7 @@ constexpr int kSelectThreads = 1024;
 constexpr int kMaxPool = 16384;         // B + T limit (selection keeps the pool in LDS)
 
 hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_attention_full_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s);
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s);
 hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride);

@@ -1,6 +1,8 @@
 // Frame refresh (Eq. 4 and Eq. 6): one launch, two kinds of workgroup.
 //
-// Workgroups 0 .. L*H_kv-1, one per (layer, KV head), refresh the compressed state:
+// Workgroups 0 .. L*H_kv-1, one per (layer, KV head), refresh the compressed state
+// (mode 0: attention-driven selection; mode 1, the recency-window baseline: the
+// same steps with the position as the selection key):
 // 1. Finalise the importance scores of the candidate pool (state slots, then the
 //    frame's tokens): s_j = (1/T) * sum over row tiles of the attention kernel's
 //    column sums, added in fixed tile order (deterministic, no atomics).
@@ -16,6 +18,7 @@
 //    K/V rows into those slots.  Retained slots never move.
 // Workgroups L*H_kv .. 2*L*H_kv-1 append the frame's K/V rows of one (layer, KV
 // head) to the decode cache D (the detailed state), concurrently with the above.
+// Mode 2 (streaming full attention, no compressed state) launches only these.
 #include "internal.h"
 
 namespace skv {
@@ -193,26 +196,29 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
   }
   __syncthreads();
 
+  // selection key: the score bits, or the position for the recency window
+  const bool recent = a.mode == 1;
+  auto key = [&](int j) -> uint32_t { return recent ? static_cast<uint32_t>(spos[j]) : sbits[j]; };
   const bool prune = P > B;
-  uint32_t s_thr = 0u;  // keep s > s_thr, and s == s_thr with position <= p_thr
+  uint32_t s_thr = 0u;  // keep key > s_thr, and key == s_thr with position <= p_thr
   int32_t p_thr = 0x7FFFFFFF;
   if (prune && B > 0) {
-    const RadixResult r = radix_select(P, B, [&](int j) { return sbits[j]; }, [&](int) { return true; }, sh);
+    const RadixResult r = radix_select(P, B, key, [&](int) { return true; }, sh);
     s_thr = r.value;
     if (r.need < r.equal) {
-      // exact ties straddle the boundary: the r.need lowest positions among s == s_thr;
+      // exact ties straddle the boundary: the r.need lowest positions among key == s_thr;
       // a complemented position makes "largest" mean "lowest position"
       const RadixResult q = radix_select(
           P, r.need, [&](int j) { return 0x7FFFFFFFu - static_cast<uint32_t>(spos[j]); },
-          [&](int j) { return sbits[j] == s_thr; }, sh);
+          [&](int j) { return key(j) == s_thr; }, sh);
       p_thr = static_cast<int32_t>(0x7FFFFFFFu - q.value);
     }
   }
   auto kept = [&](int j) -> bool {
     if (!prune) return true;
     if (B == 0) return false;
-    const uint32_t s = sbits[j];
-    return s > s_thr || (s == s_thr && spos[j] <= p_thr);
+    const uint32_t kj = key(j);
+    return kj > s_thr || (kj == s_thr && spos[j] <= p_thr);
   };
 
   // Admitted frame tokens, ascending t.
@@ -285,17 +291,18 @@ __device__ void append_frame(const RefreshArgs& a, int lg) {
 __global__ __launch_bounds__(kSelectThreads) void refresh_kernel(RefreshArgs a) {
   extern __shared__ uint32_t pool_mem[];  // [pool] score bits, then [pool] positions
   __shared__ SelectShared sh;
-  const int n_lg = a.n_layers * a.H_kv;
-  if (static_cast<int>(blockIdx.x) < n_lg) {
+  const int n_sel = a.mode == 2 ? 0 : a.n_layers * a.H_kv;
+  if (static_cast<int>(blockIdx.x) < n_sel) {
     refresh_state(a, blockIdx.x, sh, pool_mem);
   } else {
-    append_frame(a, blockIdx.x - n_lg);
+    append_frame(a, blockIdx.x - n_sel);
   }
 }
 
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s) {
-  const size_t lds = static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t);
-  hipLaunchKernelGGL(refresh_kernel, dim3(2 * a.n_layers * a.H_kv), dim3(kSelectThreads), lds, s, a);
+  const bool select = a.mode != 2;
+  const size_t lds = select ? static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t) : 0;
+  hipLaunchKernelGGL(refresh_kernel, dim3((select ? 2 : 1) * a.n_layers * a.H_kv), dim3(kSelectThreads), lds, s, a);
   return hipGetLastError();
 }
 

@@ -24,6 +24,7 @@
 namespace skv {
 hipError_t prepare_refresh(int pool_stride);
 hipError_t prepare_attention_mfma();
+hipError_t prepare_attention_full();
 }  // namespace skv
 
 namespace {
@@ -199,13 +200,18 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   if (c.pos_offset < 0) return fail(SKV_ERR_INVALID_ARG, "pos_offset must be >= 0");
   const int64_t max_tokens = static_cast<int64_t>(c.max_frames) * c.tokens_per_frame;
   if (c.pos_offset + max_tokens >= (int64_t{1} << 31)) return fail(SKV_ERR_INVALID_ARG, "positions exceed int32");
-  if (static_cast<int64_t>(c.capacity) + c.tokens_per_frame > skv::kMaxPool)
+  if (c.policy != SKV_POLICY_STATEKV && c.policy != SKV_POLICY_RECENT && c.policy != SKV_POLICY_FULL)
+    return fail(SKV_ERR_INVALID_ARG, "unknown policy");
+  if (c.reserved != 0) return fail(SKV_ERR_INVALID_ARG, "reserved must be 0");
+  const bool full = c.policy == SKV_POLICY_FULL;
+  if (!full && static_cast<int64_t>(c.capacity) + c.tokens_per_frame > skv::kMaxPool)
     return fail(SKV_ERR_UNSUPPORTED, "capacity + tokens_per_frame exceeds 16384");
   const int64_t rows = static_cast<int64_t>(c.n_q_heads / c.n_kv_heads) * c.tokens_per_frame;
   if (rows >= (int64_t{1} << 30)) return fail(SKV_ERR_INVALID_ARG, "too many query rows per KV head");
 
   skv_ctx* ctx = new skv_ctx();
   ctx->cfg = c;
+  if (full) ctx->cfg.capacity = 0;  // no compressed state: the context is the decode cache
   ctx->stream = static_cast<hipStream_t>(hip_stream);
   ctx->elem = c.dtype == SKV_BF16 ? 2 : 4;
   ctx->G = c.n_q_heads / c.n_kv_heads;
@@ -215,7 +221,7 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   ctx->use_mfma = c.dtype == SKV_BF16 && !(force_simple && force_simple[0] == '1');
   ctx->tile_stride = ctx->use_mfma ? skv::plan_max_tiles(static_cast<int>(rows), skv::kMfmaRowsPerWave, skv::kMfmaWaves)
                                   : static_cast<int>((rows + skv::kSimpleRowsPerTile - 1) / skv::kSimpleRowsPerTile);
-  ctx->pool_stride = ((c.capacity + c.tokens_per_frame + 63) / 64) * 64;
+  ctx->pool_stride = ((ctx->cfg.capacity + c.tokens_per_frame + 63) / 64) * 64;
   ctx->row_bytes = static_cast<size_t>(c.head_dim) * ctx->elem;
   ctx->max_tokens = max_tokens;
   ctx->last_pool.assign(c.n_layers, 0);
@@ -232,17 +238,18 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   }
 
   const size_t LH = static_cast<size_t>(c.n_layers) * c.n_kv_heads;
-  const size_t state_bytes = LH * c.capacity * ctx->row_bytes;
+  const size_t B_state = static_cast<size_t>(ctx->cfg.capacity);
+  const size_t state_bytes = LH * B_state * ctx->row_bytes;
   const size_t cache_bytes = LH * static_cast<size_t>(max_tokens) * ctx->row_bytes;
   struct Req { void** p; size_t bytes; };
   const Req reqs[] = {
       {&ctx->state_k, state_bytes},
       {&ctx->state_v, state_bytes},
-      {reinterpret_cast<void**>(&ctx->state_pos), LH * c.capacity * sizeof(int32_t)},
-      {reinterpret_cast<void**>(&ctx->state_score), LH * c.capacity * sizeof(float)},
+      {reinterpret_cast<void**>(&ctx->state_pos), LH * B_state * sizeof(int32_t)},
+      {reinterpret_cast<void**>(&ctx->state_score), LH * B_state * sizeof(float)},
       {&ctx->cache_k, cache_bytes},
       {&ctx->cache_v, cache_bytes},
-      {reinterpret_cast<void**>(&ctx->partial), LH * ctx->tile_stride * ctx->pool_stride * sizeof(float)},
+      {reinterpret_cast<void**>(&ctx->partial), full ? 0 : LH * ctx->tile_stride * ctx->pool_stride * sizeof(float)},
       {reinterpret_cast<void**>(&ctx->pool_score), LH * ctx->pool_stride * sizeof(float)},
       {reinterpret_cast<void**>(&ctx->pool_pos), LH * ctx->pool_stride * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_src), LH * c.tokens_per_frame * sizeof(int32_t)},
@@ -298,11 +305,19 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.q = q;
   aa.kf = k;
   aa.vf = v;
-  aa.ks = static_cast<char*>(ctx->state_k) + lh0 * B * rb;
-  aa.vs = static_cast<char*>(ctx->state_v) + lh0 * B * rb;
+  const bool full = c.policy == SKV_POLICY_FULL;
+  if (full) {  // every earlier token, from the decode cache
+    aa.ks = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
+    aa.vs = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
+    aa.kv_rows = static_cast<int>(ctx->max_tokens);
+  } else {
+    aa.ks = static_cast<char*>(ctx->state_k) + lh0 * B * rb;
+    aa.vs = static_cast<char*>(ctx->state_v) + lh0 * B * rb;
+    aa.kv_rows = B;
+  }
   aa.out = out;
   const skv_ctx::Plan& plan = ctx->plans[static_cast<size_t>(layer_count - 1)];
-  aa.partial = ctx->partial + lh0 * ctx->tile_stride * ctx->pool_stride;
+  aa.partial = full ? nullptr : ctx->partial + lh0 * ctx->tile_stride * ctx->pool_stride;
   aa.work = plan.work;
   aa.n_work = plan.n_work;
   aa.n_layers = layer_count;
@@ -311,7 +326,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.G = ctx->G;
   aa.T = T;
   aa.B = B;
-  aa.S = S;
+  aa.S = full ? static_cast<int>(ctx->frame * T) : S;
   aa.tile_stride = ctx->tile_stride;
   aa.pool_stride = ctx->pool_stride;
   aa.scale_log2 = ctx->scale_log2;
@@ -343,18 +358,20 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.row_bytes = static_cast<int>(rb);
   ra.frame_pos0 = pos0;
   ra.inv_T = 1.0f / static_cast<float>(T);
+  ra.mode = c.policy == SKV_POLICY_STATEKV ? 0 : (c.policy == SKV_POLICY_RECENT ? 1 : 2);
 
   hipError_t e = mark(0);
   if (e == hipSuccess)
-    e = ctx->use_mfma ? skv::launch_attention_mfma_bf16(aa, d, ctx->stream)
-                      : skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream);
+    e = !ctx->use_mfma ? skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream)
+        : full         ? skv::launch_attention_full_bf16(aa, d, ctx->stream)
+                       : skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
   if (e == hipSuccess) e = mark(1);
   if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
   if (e == hipSuccess) e = mark(2);
   if (e != hipSuccess) return hip_fail(e, "frame step launch");
   if (timing) ++ctx->timing_n;
 
-  for (int l = layer_begin; l < layer_begin + layer_count; ++l) ctx->last_pool[l] = S + T;
+  for (int l = layer_begin; l < layer_begin + layer_count; ++l) ctx->last_pool[l] = full ? 0 : S + T;
   ctx->next_layer += layer_count;
   if (ctx->next_layer == c.n_layers) {
     ctx->next_layer = 0;
@@ -465,6 +482,8 @@ hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride) {
   hipError_t e = prepare_refresh(pool_stride);
   if (e != hipSuccess) return e;
   if (bf16) e = prepare_attention_mfma();
+  if (e != hipSuccess) return e;
+  if (bf16) e = prepare_attention_full();
   return e;
 }
 

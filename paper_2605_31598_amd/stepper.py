@@ -18,7 +18,7 @@ class FrameStepper:
     """One video stream: compressed state and decode cache of every layer."""
 
     def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
-                 dtype="bf16", softmax_scale=0.0, pos_offset=0, stream=None):
+                 dtype="bf16", softmax_scale=0.0, pos_offset=0, stream=None, policy="statekv"):
         import torch
 
         if not torch.cuda.is_available():
@@ -29,16 +29,18 @@ class FrameStepper:
         self.torch_dtype = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.np_dtype = np.uint16 if dtype == "bf16" else np.float32
         self.elem = 2 if dtype == "bf16" else 4
+        self.policy = policy
         self.cfg = B.skv_config(n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
-                                _DTYPES[dtype], softmax_scale, pos_offset)
+                                _DTYPES[dtype], softmax_scale, pos_offset, B.POLICIES[policy], 0)
         self.n_layers, self.H_q, self.H_kv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
-        self.T, self.B, self.max_frames = tokens_per_frame, capacity, max_frames
+        # streaming full attention keeps no compressed state
+        self.T, self.B, self.max_frames = tokens_per_frame, (0 if policy == "full" else capacity), max_frames
         self.ctx = B.skv_init(self.cfg, self.stream.cuda_stream)
 
     @classmethod
-    def from_workload(cls, wl, max_frames=None, stream=None):
+    def from_workload(cls, wl, max_frames=None, stream=None, policy="statekv"):
         return cls(wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.tokens_per_frame, wl.capacity,
-                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream)
+                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream, policy)
 
     # ------------------------------------------------------------------ step
     def _check(self, name, t, heads, n_layers):
@@ -115,6 +117,19 @@ class FrameStepper:
                 arr[g] = B.copy_to_host(base + g * M * d * self.elem, n * d * self.elem).view(self.np_dtype).reshape(n, d)
             out.append(arr)
         return out[0], out[1], cv.n_tokens
+
+    def write_cache(self, layer, k, v):
+        """Overwrite decode-cache rows 0..n-1 of every KV head (k, v [H_kv, n, d] in storage
+        form), e.g. to give a streaming-full-attention step a history without running it."""
+        self._sync()
+        cv = B.skv_decode_cache_view(self.ctx, layer)
+        H, d, M = self.H_kv, self.d, cv.max_tokens
+        n = k.shape[1]
+        if k.shape != (H, n, d) or v.shape != (H, n, d) or n > M:
+            raise ValueError(f"cache rows must be [{H}][n <= {M}][{d}]")
+        for base, arr in ((cv.k, k), (cv.v, v)):
+            for g in range(H):
+                B.copy_to_device(base + g * M * d * self.elem, np.ascontiguousarray(arr[g], dtype=self.np_dtype))
 
     # ------------------------------------------------------------ timing
     def timing_start(self, max_steps):

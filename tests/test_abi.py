@@ -53,7 +53,7 @@ def test_struct_layouts_match_header(tmp_path):
 int main(void) {
   F(skv_config, n_layers) F(skv_config, n_q_heads) F(skv_config, n_kv_heads) F(skv_config, head_dim)
   F(skv_config, tokens_per_frame) F(skv_config, capacity) F(skv_config, max_frames) F(skv_config, dtype)
-  F(skv_config, softmax_scale) F(skv_config, pos_offset)
+  F(skv_config, softmax_scale) F(skv_config, pos_offset) F(skv_config, policy) F(skv_config, reserved)
   F(skv_state_view_t, k) F(skv_state_view_t, v) F(skv_state_view_t, pos) F(skv_state_view_t, score)
   F(skv_state_view_t, size) F(skv_state_view_t, capacity) F(skv_state_view_t, frame)
   F(skv_state_view_t, pool_score) F(skv_state_view_t, pool_pos) F(skv_state_view_t, pool_size)
@@ -95,6 +95,9 @@ def _cfg(**kw):
     (dict(capacity=16000, tokens_per_frame=729), B.SKV_ERR_UNSUPPORTED),
     (dict(max_frames=2 ** 30, tokens_per_frame=4), B.SKV_ERR_INVALID_ARG),
     (dict(pos_offset=-3), B.SKV_ERR_INVALID_ARG),
+    (dict(policy=3), B.SKV_ERR_INVALID_ARG),
+    (dict(policy=-1), B.SKV_ERR_INVALID_ARG),
+    (dict(reserved=1), B.SKV_ERR_INVALID_ARG),
 ])
 def test_init_rejects_bad_configs_before_touching_the_device(lib, kw, status):
     h = ctypes.c_void_p(123)
