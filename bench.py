@@ -94,6 +94,54 @@ def refresh_bytes(wl, S, n_qtiles, admitted):
     return select + update + append
 
 
+def full_attention_flops(wl, n):
+    """Causal-exact FLOPs of frame n under streaming full attention (all n*T earlier tokens)."""
+    return attention_flops(wl, n * wl.tokens_per_frame)
+
+
+def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
+    """The paper's two comparison systems on the same resident inputs, outside the timed
+    region of the main line: streaming full attention over the decode cache (one whole
+    video, per-frame times) and the recency window of B tokens (one video)."""
+    from paper_2605_31598_amd import FrameStepper
+    import torch
+
+    N, T = wl.n_frames, wl.tokens_per_frame
+    res = {}
+    for policy in ("full", "recent"):
+        st = FrameStepper.from_workload(wl, stream=stream, policy=policy)
+        try:
+            for f in range(4):  # warm the kernels, then restart the stream
+                st.step(q_all[f], k_all[f], v_all[f], out)
+            st.reset()
+            torch.cuda.synchronize()
+            st.timing_start(N)
+            t0 = time.perf_counter()
+            for f in range(N):
+                st.step(q_all[f], k_all[f], v_all[f], out)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            ms = st.timing_stop(N).astype(np.float64)
+        finally:
+            st.close()
+        frame_ms = ms.sum(axis=1)
+        entry = {"frames_per_s": round(N / wall, 2), "video_s": round(wall, 3),
+                 "frame_ms_at": {str(f): round(float(frame_ms[f]), 4) for f in (0, 11, 64, 128, 256, N - 1) if f < N}}
+        if policy == "full":
+            alg = np.array([full_attention_flops(wl, f) for f in range(N)], dtype=np.float64)
+            last = slice(N - 64, N)
+            entry["attention_tflops_last_64_frames"] = round(float(alg[last].sum() / (ms[last, 0].sum() * 1e-3) / 1e12), 1)
+            entry["attention_frac_of_bf16_peak_last_64"] = round(float(alg[last].sum() / (ms[last, 0].sum() * 1e-3) / 1e12)
+                                                                 / PEAK_BF16_TFLOPS, 4)
+            slower = np.nonzero(frame_ms > statekv_ms)[0]
+            entry["crossover_frame"] = int(slower[0]) if slower.size else None
+            entry["statekv_speedup_at_last_frame"] = round(float(frame_ms[-1] / statekv_ms), 2)
+        res[policy] = entry
+        print(f"[bench] {policy}: {entry['frames_per_s']} frames/s over one video", file=sys.stderr, flush=True)
+    res["statekv_frame_ms_state_full"] = round(statekv_ms, 4)
+    return res
+
+
 def cpu_baseline(wl, seconds):
     """The fp64 oracle on a bounded sample: layer 0, frames from state-full onward, on a
     full state of the most recent tokens; scaled to frames/s of the whole stack."""
@@ -147,6 +195,8 @@ def main():
     ap.add_argument("--workload", default="vlm7b_28layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-baselines", action="store_true",
+                    help="skip the Full SA and recency-window runs reported beside the main line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -283,6 +333,8 @@ def main():
             "from_frame": int(wl.full_from_frame),
         },
     }
+    if not args.no_baselines:
+        result["baselines"] = baselines(wl, q_all, k_all, v_all, out, stream, med)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
