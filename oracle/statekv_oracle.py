@@ -252,6 +252,28 @@ def run_layer(inputs, n_frames, capacity, n_kv_heads, head_dim, scale=None, pos_
     return st, cache, results
 
 
+def decode_attention(q, k_hist, v_hist, k_new, v_new, scale=None):
+    """Decoding after (or between) frames reads the detailed state D, not C (the decoding
+    paragraph): the t new tokens attend to every earlier token of D (the video's tokens, then
+    the tokens decoded before), all visible, and to the new tokens up to themselves (causal).
+    That is Eq. 5 with the whole history as the memory.
+
+    q [H_q, t, d]; k_hist, v_hist [H_kv, n, d]; k_new, v_new [H_kv, t, d].  Returns [H_q, t, d]."""
+    H_q, t, d = q.shape
+    H_kv = k_new.shape[0]
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    n = k_hist.shape[1]
+    k_pool = np.concatenate([k_hist, k_new], axis=1)
+    v_pool = np.concatenate([v_hist, v_new], axis=1)
+    out = np.empty_like(q)
+    grp = kv_head_of(H_q, H_kv)
+    for g in range(H_kv):
+        hs = np.nonzero(grp == g)[0]
+        out[hs] = frame_attention(q[hs], k_pool[g:g + 1], v_pool[g:g + 1], n, scale)[0]
+    return out
+
+
 def attention_flops(n_q_heads, head_dim, tokens_per_frame, n_state):
     """Closed form of StepResult.flops: 4*d*H_q*(T*S + T(T+1)/2)."""
     T = tokens_per_frame

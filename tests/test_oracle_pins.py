@@ -168,6 +168,25 @@ def check_recent_policy_window(seed=6, H_q=4, H_kv=2, d=8, T=5, N=6, B=7, pos_of
         st = r.state
 
 
+def check_decode_is_causal_sdpa(seed=8, H_q=6, H_kv=2, d=8, T=4, N=3, chunks=(1, 3, 1)):
+    """Decoding over D: after N frames, chunks of t new tokens; every decoded token's output
+    equals one causal attention over the whole stream (video tokens, then decoded tokens)."""
+    rng = np.random.default_rng(seed)
+    n_dec = sum(chunks)
+    L = N * T + n_dec
+    q = rng.standard_normal((H_q, L, d))
+    k = rng.standard_normal((H_kv, L, d))
+    v = rng.standard_normal((H_kv, L, d))
+    scale = d ** -0.5
+    ref = sdpa_causal(q, k, v, scale)
+    pos = N * T
+    for t in chunks:
+        new = slice(pos, pos + t)
+        o = orc.decode_attention(q[:, new], k[:, :pos], v[:, :pos], k[:, new], v[:, new], scale)
+        np.testing.assert_allclose(o, ref[:, new], rtol=0, atol=1e-12)
+        pos += t
+
+
 def check_zero_query_closed_form(H_q=6, H_kv=3, d=4, T=5, N=6, B=7):
     G = H_q // H_kv
     rng = np.random.default_rng(3)
@@ -212,6 +231,11 @@ def test_full_policy_equals_causal_sdpa_over_the_stream():
 def test_recent_policy_keeps_the_last_tokens():
     check_recent_policy_window()
     check_recent_policy_window(seed=7, T=4, B=8, N=5, pos_offset=0)  # window of whole frames
+
+
+def test_decode_over_the_detailed_cache_equals_causal_sdpa():
+    check_decode_is_causal_sdpa()
+    check_decode_is_causal_sdpa(seed=9, H_q=7, H_kv=1, d=16, T=5, N=2, chunks=(4, 2))
 
 
 def test_golden_handworked():
@@ -406,7 +430,7 @@ PINS = [check_golden, check_full_capacity_is_causal_sdpa,
         lambda: check_full_capacity_is_causal_sdpa(seed=11, H_q=14, H_kv=2, d=16, T=7, N=3),
         check_zero_capacity_is_framewise_sdpa, check_zero_query_closed_form,
         lambda: check_bruteforce(1, 4, 2, 4, 4, 3, 4, 5), check_full_policy_is_causal_sdpa,
-        check_recent_policy_window]
+        check_recent_policy_window, check_decode_is_causal_sdpa]
 
 
 @pytest.mark.parametrize("name,attr,mutant", [
