@@ -78,7 +78,7 @@ typedef struct {
   float softmax_scale;      /* logit scale; 0 selects 1/sqrt(head_dim) */
   int64_t pos_offset;       /* virtual position of the first video token (room for a text prefix) */
   int32_t policy;           /* skv_policy; 0 (a zeroed config) is StateKV */
-  int32_t reserved;         /* must be 0 */
+  int32_t max_decode_tokens; /* rows of D kept for tokens decoded after the video (>= 0) */
 } skv_config;
 
 typedef struct skv_ctx skv_ctx;
@@ -86,8 +86,8 @@ typedef struct skv_ctx skv_ctx;
 /* Validates cfg, allocates and zeroes every device buffer of one video stream
  * (compressed state and decode cache of all layers, scratch), and binds the
  * context to hip_stream (a hipStream_t; NULL means the default stream).
- * Limits: pos_offset + max_frames * T < 2^31; B + T <= 16384 (STATEKV and
- * RECENT); policy one of skv_policy and reserved = 0, else SKV_ERR_INVALID_ARG.
+ * Limits: pos_offset + max_frames * T + max_decode_tokens < 2^31; B + T <= 16384
+ * (STATEKV and RECENT); policy one of skv_policy, else SKV_ERR_INVALID_ARG.
  * Returns SKV_OK and *out, or an error and *out = NULL. */
 skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
 
@@ -107,6 +107,25 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
  * SKV_ERR_ORDER, SKV_ERR_CAPACITY (n >= max_frames), SKV_ERR_DEVICE. */
 skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count,
                           const void* q, const void* k, const void* v, void* out);
+
+/* Decoding after (or between) frames reads the detailed state D, not C (the
+ * decoding paragraph of the method).  Runs layers [layer_begin, layer_begin +
+ * layer_count) for n_tokens new tokens: each attends to every video token of
+ * D (T * frames done), every token decoded before, and the new tokens up to
+ * itself (causal), with the grouped-query mapping of skv_frame_step; then the
+ * new tokens' K/V are appended to D's decode rows.  Split-key ("flash
+ * decoding") kernel plus a combine kernel; the whole read of D is the cost.
+ * Layers must be stepped in order, and not while a frame is half done; the
+ * decode counter advances after the last layer.
+ * Device layouts (row-major, dtype of the config):
+ *   q   [layer_count][H_q ][n_tokens][d]
+ *   k,v [layer_count][H_kv][n_tokens][d]
+ *   out [layer_count][H_q ][n_tokens][d]
+ * Errors: SKV_ERR_INVALID_ARG, SKV_ERR_ORDER, SKV_ERR_CAPACITY (more than
+ * max_decode_tokens decoded tokens), SKV_ERR_UNSUPPORTED (fp32 contexts),
+ * SKV_ERR_DEVICE. */
+skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, int32_t n_tokens,
+                           const void* q, const void* k, const void* v, void* out);
 
 /* Borrowed view of one layer's compressed state C (Eq. 4) and of the last
  * step's candidate pool.  Slots are unordered; pos gives each slot's virtual
@@ -131,38 +150,42 @@ typedef struct {
 
 skv_status skv_state_view(skv_ctx* ctx, int32_t layer, skv_state_view_t* out);
 
-/* Borrowed view of one layer's decode cache D (Eq. 4): token rows in stream
- * order, row r of KV head g at k + (g * max_tokens + r) * d.  Valid until
- * skv_destroy. */
+/* Borrowed view of one layer's decode cache D (Eq. 4): video token rows in
+ * stream order, then the rows of tokens decoded after the video; row r of KV
+ * head g at k + (g * max_tokens + r) * d.  Valid until skv_destroy. */
 typedef struct {
-  void* k;            /* [H_kv][max_tokens][d] */
-  void* v;            /* [H_kv][max_tokens][d] */
-  int64_t n_tokens;   /* rows written = T * frames done by this layer */
-  int64_t max_tokens; /* T * max_frames */
+  void* k;               /* [H_kv][max_tokens][d] */
+  void* v;               /* [H_kv][max_tokens][d] */
+  int64_t n_tokens;      /* video rows written = T * frames done by this layer */
+  int64_t max_tokens;    /* row stride: T * max_frames + max_decode_tokens */
   int32_t n_kv_heads;
   int32_t head_dim;
+  int64_t decode_row0;   /* first decode row = T * max_frames */
+  int64_t decode_tokens; /* decode rows written by this layer */
 } skv_cache_view_t;
 
 skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* out);
 
-/* Starts a new video on the same context: frame counter and L_n return to 0,
- * every state becomes empty.  Device contents are left as they are (nothing
- * is enqueued). */
+/* Starts a new video on the same context: frame counter, decoded-token count
+ * and L_n return to 0, every state becomes empty.  Device contents are left as
+ * they are (nothing is enqueued). */
 skv_status skv_reset(skv_ctx* ctx);
 
 /* Sets the frame counter to `frame` (0 <= frame < max_frames) at layer 0, so
  * that a caller can force a state through skv_state_view and run one step
- * from it.  The state size becomes min(B, T * frame). */
+ * from it.  The state size becomes min(B, T * frame); the decoded-token count
+ * becomes 0. */
 skv_status skv_seek(skv_ctx* ctx, int64_t frame);
 
 /* Kernel timing with HIP events on the context's stream.  skv_timing_start
- * creates events for up to max_steps subsequent skv_frame_step calls (created
- * here, never in the step).  skv_timing_stop synchronises the stream and
+ * creates events for up to max_steps subsequent skv_frame_step or
+ * skv_decode_step calls (created here, never in the step).  skv_timing_stop synchronises the stream and
  * writes ms[i * SKV_N_STAGES + s] for step i and stage s, *n_steps the number
  * of steps recorded, then releases the events.  Stages: the attention launch
  * (attention and column sums of P), and the refresh launch (score
  * finalisation, Top-B selection and state update, with the decode-cache append
- * running in the same launch). */
+ * running in the same launch).  For skv_decode_step: the split-key attention
+ * with its combine, and the append. */
 enum { SKV_STAGE_ATTENTION = 0, SKV_STAGE_REFRESH = 1, SKV_N_STAGES = 2 };
 skv_status skv_timing_start(skv_ctx* ctx, int32_t max_steps);
 skv_status skv_timing_stop(skv_ctx* ctx, int32_t* n_steps, float* ms, int32_t ms_capacity);

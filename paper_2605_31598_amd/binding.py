@@ -35,7 +35,7 @@ STAGES = ("attention", "refresh")
 
 # Every symbol declared in include/statekv.h.
 EXPORTS = (
-    "skv_init", "skv_frame_step", "skv_state_view", "skv_decode_cache_view", "skv_reset", "skv_seek",
+    "skv_init", "skv_frame_step", "skv_decode_step", "skv_state_view", "skv_decode_cache_view", "skv_reset", "skv_seek",
     "skv_timing_start", "skv_timing_stop", "skv_destroy", "skv_status_string", "skv_last_error",
 )
 
@@ -45,7 +45,7 @@ class skv_config(ctypes.Structure):
         ("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
         ("head_dim", ctypes.c_int32), ("tokens_per_frame", ctypes.c_int32), ("capacity", ctypes.c_int32),
         ("max_frames", ctypes.c_int32), ("dtype", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
-        ("pos_offset", ctypes.c_int64), ("policy", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("pos_offset", ctypes.c_int64), ("policy", ctypes.c_int32), ("max_decode_tokens", ctypes.c_int32),
     ]
 
 
@@ -61,7 +61,8 @@ class skv_state_view_t(ctypes.Structure):
 class skv_cache_view_t(ctypes.Structure):
     _fields_ = [
         ("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("n_tokens", ctypes.c_int64), ("max_tokens", ctypes.c_int64),
-        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("decode_row0", ctypes.c_int64),
+        ("decode_tokens", ctypes.c_int64),
     ]
 
 
@@ -88,6 +89,8 @@ def load_library(path: str = LIB_PATH):
     lib.skv_init.argtypes = [P(skv_config), ctypes.c_void_p, P(ctypes.c_void_p)]
     lib.skv_frame_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.skv_decode_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.skv_state_view.argtypes = [ctypes.c_void_p, ctypes.c_int32, P(skv_state_view_t)]
     lib.skv_decode_cache_view.argtypes = [ctypes.c_void_p, ctypes.c_int32, P(skv_cache_view_t)]
     lib.skv_reset.argtypes = [ctypes.c_void_p]
@@ -140,6 +143,14 @@ def skv_frame_step(ctx: int, layer_begin: int, layer_count: int, q: int, k: int,
     _check(load_library().skv_frame_step(ctypes.c_void_p(ctx), layer_begin, layer_count, ctypes.c_void_p(q),
                                          ctypes.c_void_p(k), ctypes.c_void_p(v), ctypes.c_void_p(out)),
            "skv_frame_step")
+
+
+def skv_decode_step(ctx: int, layer_begin: int, layer_count: int, n_tokens: int, q: int, k: int, v: int,
+                    out: int) -> None:
+    _check(load_library().skv_decode_step(ctypes.c_void_p(ctx), layer_begin, layer_count, n_tokens,
+                                          ctypes.c_void_p(q), ctypes.c_void_p(k), ctypes.c_void_p(v),
+                                          ctypes.c_void_p(out)),
+           "skv_decode_step")
 
 
 def skv_state_view(ctx: int, layer: int) -> skv_state_view_t:

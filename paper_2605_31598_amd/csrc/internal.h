@@ -55,6 +55,32 @@ struct RefreshArgs {
   int mode;                  // 0: Top-B by score, 1: the B most recent, 2: append only
 };
 
+// Decode over the detailed cache (split-key flash decoding).  Each wave of the
+// split kernel owns one item = (layer-head, 32-row block, key split); the
+// combine kernel merges the splits of every row.
+struct DecodeArgs {
+  const void* q;       // [n_layers][H_q][t][d]   new tokens' queries
+  const void* kn;      // [n_layers][H_kv][t][d]  new tokens' keys
+  const void* vn;      // [n_layers][H_kv][t][d]  new tokens' values
+  const void* ck;      // [n_layers][H_kv][max_tokens][d]  decode cache D
+  const void* cv;
+  void* out;           // [n_layers][H_q][t][d]
+  float* part_o;       // [n_items][32][d]  unnormalised output of each split
+  float* part_ml;      // [n_items][2][32]  row maximum (logit units), row sum
+  int64_t max_tokens;  // row stride of D
+  int64_t dec_row0;    // first decode row of D
+  int n_layers, H_q, H_kv, G, t;
+  int S;               // video tokens of D (T * frames done)
+  int n_dec;           // tokens decoded before this call
+  int n_rb;            // 32-row blocks per layer-head: ceil(G t / 32)
+  int split;           // keys per split, a multiple of 32
+  int n_split;         // ceil((S + n_dec + t) / split)
+  float scale_log2;
+};
+
+constexpr int kDecodeMaxTokens = 64;  // new tokens per decode call
+constexpr int kDecodeItems = 8192;    // split items aimed at per call (partials sized for it)
+
 constexpr int kMfmaRowsPerWave = 32;    // query rows (G*T packed) per attention wave
 constexpr int kMfmaWaves = 8;           // waves per attention workgroup (at most)
 constexpr int kSimpleRowsPerTile = 64;
@@ -64,6 +90,7 @@ constexpr int kMaxPool = 16384;         // B + T limit (selection keeps the pool
 hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_full_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s);
+hipError_t launch_decode_bf16(const DecodeArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s);
 hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride);
 

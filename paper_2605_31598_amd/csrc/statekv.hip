@@ -14,6 +14,7 @@
 
 #include <cmath>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -68,6 +69,10 @@ struct skv_ctx {
   int32_t* pool_pos = nullptr;
   int32_t* admit_src = nullptr;    // [L][H_kv][T]
   int32_t* admit_dst = nullptr;
+  float* dec_part_o = nullptr;     // decode split partials: [dec_items][32][d]
+  float* dec_part_ml = nullptr;    // [dec_items][2][32]
+  int dec_items = 0;
+  int64_t dec_row0 = 0;            // first decode row of D
   // attention work plans, one per layer_count (index layer_count - 1), in one
   // device allocation; the fp32 path uses fixed 64-row tiles instead
   struct Plan {
@@ -81,6 +86,9 @@ struct skv_ctx {
   // progress of the stream
   int64_t frame = 0;    // frame being processed
   int next_layer = 0;   // next layer expected within that frame
+  int64_t n_decoded = 0;   // tokens decoded after the video (all layers done)
+  int dec_next_layer = 0;  // next layer expected within the current decode call
+  int dec_pending = 0;     // tokens of the decode call in progress
   std::vector<int32_t> last_pool;  // candidates of each layer's last step
 
   // timing
@@ -198,11 +206,12 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   if (!(c.softmax_scale >= 0.f) || !std::isfinite(c.softmax_scale))
     return fail(SKV_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0");
   if (c.pos_offset < 0) return fail(SKV_ERR_INVALID_ARG, "pos_offset must be >= 0");
-  const int64_t max_tokens = static_cast<int64_t>(c.max_frames) * c.tokens_per_frame;
+  if (c.max_decode_tokens < 0) return fail(SKV_ERR_INVALID_ARG, "max_decode_tokens must be >= 0");
+  const int64_t video_tokens = static_cast<int64_t>(c.max_frames) * c.tokens_per_frame;
+  const int64_t max_tokens = video_tokens + c.max_decode_tokens;
   if (c.pos_offset + max_tokens >= (int64_t{1} << 31)) return fail(SKV_ERR_INVALID_ARG, "positions exceed int32");
   if (c.policy != SKV_POLICY_STATEKV && c.policy != SKV_POLICY_RECENT && c.policy != SKV_POLICY_FULL)
     return fail(SKV_ERR_INVALID_ARG, "unknown policy");
-  if (c.reserved != 0) return fail(SKV_ERR_INVALID_ARG, "reserved must be 0");
   const bool full = c.policy == SKV_POLICY_FULL;
   if (!full && static_cast<int64_t>(c.capacity) + c.tokens_per_frame > skv::kMaxPool)
     return fail(SKV_ERR_UNSUPPORTED, "capacity + tokens_per_frame exceeds 16384");
@@ -224,6 +233,13 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   ctx->pool_stride = ((ctx->cfg.capacity + c.tokens_per_frame + 63) / 64) * 64;
   ctx->row_bytes = static_cast<size_t>(c.head_dim) * ctx->elem;
   ctx->max_tokens = max_tokens;
+  ctx->dec_row0 = video_tokens;
+  if (c.max_decode_tokens > 0 && c.dtype == SKV_BF16) {
+    const int64_t t_max = c.max_decode_tokens < skv::kDecodeMaxTokens ? c.max_decode_tokens : skv::kDecodeMaxTokens;
+    const int64_t rb_max = (ctx->G * t_max + 31) / 32;
+    const int64_t need = static_cast<int64_t>(c.n_layers) * c.n_kv_heads * rb_max;
+    ctx->dec_items = static_cast<int>(need > skv::kDecodeItems ? need : skv::kDecodeItems);
+  }
   ctx->last_pool.assign(c.n_layers, 0);
 
   hipError_t e = hipGetDevice(&ctx->device);
@@ -254,6 +270,8 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
       {reinterpret_cast<void**>(&ctx->pool_pos), LH * ctx->pool_stride * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_src), LH * c.tokens_per_frame * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_dst), LH * c.tokens_per_frame * sizeof(int32_t)},
+      {reinterpret_cast<void**>(&ctx->dec_part_o), static_cast<size_t>(ctx->dec_items) * 32 * c.head_dim * sizeof(float)},
+      {reinterpret_cast<void**>(&ctx->dec_part_ml), static_cast<size_t>(ctx->dec_items) * 64 * sizeof(float)},
   };
   for (const Req& r : reqs) {
     const skv_status s = alloc(ctx, r.bytes, r.p);
@@ -289,6 +307,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
     return fail(SKV_ERR_INVALID_ARG, "layer range outside [0, n_layers)");
   if (layer_begin != ctx->next_layer)
     return fail(SKV_ERR_ORDER, "expected layer_begin = " + std::to_string(ctx->next_layer));
+  if (ctx->dec_next_layer != 0) return fail(SKV_ERR_ORDER, "a decode call is half done");
   if (ctx->frame >= c.max_frames) return fail(SKV_ERR_CAPACITY, "decode cache is full (max_frames reached)");
 
   const int T = c.tokens_per_frame, Hkv = c.n_kv_heads, B = c.capacity, d = c.head_dim;
@@ -380,6 +399,94 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   return SKV_OK;
 }
 
+skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, int32_t n_tokens,
+                           const void* q, const void* k, const void* v, void* out) {
+  if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr)
+    return fail(SKV_ERR_INVALID_ARG, "q, k, v and out must be device pointers");
+  const skv_config& c = ctx->cfg;
+  if (layer_count < 1 || layer_begin < 0 || layer_begin + layer_count > c.n_layers)
+    return fail(SKV_ERR_INVALID_ARG, "layer range outside [0, n_layers)");
+  if (n_tokens < 1 || n_tokens > skv::kDecodeMaxTokens)
+    return fail(SKV_ERR_INVALID_ARG, "n_tokens must be in [1, " + std::to_string(skv::kDecodeMaxTokens) + "]");
+  if (c.dtype != SKV_BF16) return fail(SKV_ERR_UNSUPPORTED, "decoding is implemented for bf16 contexts");
+  if (ctx->next_layer != 0) return fail(SKV_ERR_ORDER, "a frame is half done");
+  if (layer_begin != ctx->dec_next_layer)
+    return fail(SKV_ERR_ORDER, "expected layer_begin = " + std::to_string(ctx->dec_next_layer));
+  if (ctx->dec_next_layer != 0 && n_tokens != ctx->dec_pending)
+    return fail(SKV_ERR_INVALID_ARG, "n_tokens differs from the decode call in progress");
+  if (ctx->n_decoded + n_tokens > c.max_decode_tokens)
+    return fail(SKV_ERR_CAPACITY, "more tokens than max_decode_tokens");
+
+  const int Hkv = c.n_kv_heads, d = c.head_dim, t = n_tokens;
+  const size_t lh0 = static_cast<size_t>(layer_begin) * Hkv;
+  const size_t rb = ctx->row_bytes;
+  const int S = static_cast<int>(ctx->frame * c.tokens_per_frame);
+  const int n_dec = static_cast<int>(ctx->n_decoded);
+  const int n_keys = S + n_dec + t;
+  const int LH = layer_count * Hkv;
+  const int n_rb = (ctx->G * t + 31) / 32;
+  const int per = std::max(1, ctx->dec_items / (LH * n_rb));  // splits per (layer-head, row block)
+  const int split = std::max(256, ((n_keys + per - 1) / per + 31) / 32 * 32);
+
+  skv::DecodeArgs da;
+  da.q = q;
+  da.kn = k;
+  da.vn = v;
+  da.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
+  da.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
+  da.out = out;
+  da.part_o = ctx->dec_part_o;
+  da.part_ml = ctx->dec_part_ml;
+  da.max_tokens = ctx->max_tokens;
+  da.dec_row0 = ctx->dec_row0;
+  da.n_layers = layer_count;
+  da.H_q = c.n_q_heads;
+  da.H_kv = Hkv;
+  da.G = ctx->G;
+  da.t = t;
+  da.S = S;
+  da.n_dec = n_dec;
+  da.n_rb = n_rb;
+  da.split = split;
+  da.n_split = (n_keys + split - 1) / split;
+  da.scale_log2 = ctx->scale_log2;
+
+  // append of the new tokens' K/V to D's decode rows (the refresh kernel's append-only mode)
+  skv::RefreshArgs ra{};
+  ra.kf = k;
+  ra.vf = v;
+  ra.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
+  ra.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
+  ra.max_tokens = ctx->max_tokens;
+  ra.first_row = ctx->dec_row0 + n_dec;
+  ra.n_layers = layer_count;
+  ra.H_kv = Hkv;
+  ra.T = t;
+  ra.row_bytes = static_cast<int>(rb);
+  ra.mode = 2;
+
+  const bool timing = ctx->timing_n < ctx->timing_max;
+  hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
+  auto mark = [&](int i) -> hipError_t { return timing ? hipEventRecord(ev[i], ctx->stream) : hipSuccess; };
+  hipError_t e = mark(0);
+  if (e == hipSuccess) e = skv::launch_decode_bf16(da, d, ctx->stream);
+  if (e == hipSuccess) e = mark(1);
+  if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
+  if (e == hipSuccess) e = mark(2);
+  if (e != hipSuccess) return hip_fail(e, "decode step launch");
+  if (timing) ++ctx->timing_n;
+
+  ctx->dec_pending = t;
+  ctx->dec_next_layer += layer_count;
+  if (ctx->dec_next_layer == c.n_layers) {
+    ctx->dec_next_layer = 0;
+    ctx->n_decoded += t;
+    ctx->dec_pending = 0;
+  }
+  return SKV_OK;
+}
+
 skv_status skv_state_view(skv_ctx* ctx, int32_t layer, skv_state_view_t* out) {
   if (ctx == nullptr || out == nullptr) return fail(SKV_ERR_INVALID_ARG, "NULL argument");
   const skv_config& c = ctx->cfg;
@@ -411,6 +518,8 @@ skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* 
   out->max_tokens = ctx->max_tokens;
   out->n_kv_heads = c.n_kv_heads;
   out->head_dim = c.head_dim;
+  out->decode_row0 = ctx->dec_row0;
+  out->decode_tokens = ctx->n_decoded + (layer < ctx->dec_next_layer ? ctx->dec_pending : 0);
   return SKV_OK;
 }
 
@@ -418,6 +527,9 @@ skv_status skv_reset(skv_ctx* ctx) {
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
   ctx->frame = 0;
   ctx->next_layer = 0;
+  ctx->n_decoded = 0;
+  ctx->dec_next_layer = 0;
+  ctx->dec_pending = 0;
   std::fill(ctx->last_pool.begin(), ctx->last_pool.end(), 0);
   return SKV_OK;
 }
@@ -427,6 +539,9 @@ skv_status skv_seek(skv_ctx* ctx, int64_t frame) {
   if (frame < 0 || frame >= ctx->cfg.max_frames) return fail(SKV_ERR_INVALID_ARG, "frame out of range");
   ctx->frame = frame;
   ctx->next_layer = 0;
+  ctx->n_decoded = 0;
+  ctx->dec_next_layer = 0;
+  ctx->dec_pending = 0;
   return SKV_OK;
 }
 

@@ -18,7 +18,8 @@ class FrameStepper:
     """One video stream: compressed state and decode cache of every layer."""
 
     def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
-                 dtype="bf16", softmax_scale=0.0, pos_offset=0, stream=None, policy="statekv"):
+                 dtype="bf16", softmax_scale=0.0, pos_offset=0, stream=None, policy="statekv",
+                 max_decode_tokens=0):
         import torch
 
         if not torch.cuda.is_available():
@@ -31,16 +32,16 @@ class FrameStepper:
         self.elem = 2 if dtype == "bf16" else 4
         self.policy = policy
         self.cfg = B.skv_config(n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
-                                _DTYPES[dtype], softmax_scale, pos_offset, B.POLICIES[policy], 0)
+                                _DTYPES[dtype], softmax_scale, pos_offset, B.POLICIES[policy], max_decode_tokens)
         self.n_layers, self.H_q, self.H_kv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         # streaming full attention keeps no compressed state
         self.T, self.B, self.max_frames = tokens_per_frame, (0 if policy == "full" else capacity), max_frames
         self.ctx = B.skv_init(self.cfg, self.stream.cuda_stream)
 
     @classmethod
-    def from_workload(cls, wl, max_frames=None, stream=None, policy="statekv"):
+    def from_workload(cls, wl, max_frames=None, stream=None, policy="statekv", max_decode_tokens=0):
         return cls(wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.tokens_per_frame, wl.capacity,
-                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream, policy)
+                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream, policy, max_decode_tokens)
 
     # ------------------------------------------------------------------ step
     def _check(self, name, t, heads, n_layers):
@@ -56,6 +57,31 @@ class FrameStepper:
         self._check("v", v, self.H_kv, lc)
         self._check("out", out, self.H_q, lc)
         B.skv_frame_step(self.ctx, layer_begin, lc, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr())
+
+    def decode(self, q, k, v, out, layer_begin=0, layer_count=None):
+        """Decode step over the detailed cache: q/out [layers][H_q][t][d], k/v [layers][H_kv][t][d]."""
+        lc = self.n_layers - layer_begin if layer_count is None else layer_count
+        t = q.shape[-2]
+        for name, x, heads in (("q", q, self.H_q), ("k", k, self.H_kv), ("v", v, self.H_kv), ("out", out, self.H_q)):
+            if x.device.type != "cuda" or x.dtype != self.torch_dtype or not x.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous {self.torch_dtype} CUDA tensor")
+            if x.numel() != lc * heads * t * self.d:
+                raise ValueError(f"{name} has {x.numel()} elements, expected [{lc}][{heads}][{t}][{self.d}]")
+        B.skv_decode_step(self.ctx, layer_begin, lc, t, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr())
+
+    def read_decode_rows(self, layer):
+        """Host copy of the decode rows of one layer's cache: (k, v) [H_kv, n, d]."""
+        self._sync()
+        cv = B.skv_decode_cache_view(self.ctx, layer)
+        H, d, M, n, r0 = self.H_kv, self.d, cv.max_tokens, cv.decode_tokens, cv.decode_row0
+        out = []
+        for base in (cv.k, cv.v):
+            arr = np.empty((H, n, d), dtype=self.np_dtype)
+            for g in range(H):
+                arr[g] = B.copy_to_host(base + (g * M + r0) * d * self.elem, n * d * self.elem).view(
+                    self.np_dtype).reshape(n, d)
+            out.append(arr)
+        return out[0], out[1]
 
     def reset(self):
         B.skv_reset(self.ctx)

@@ -53,13 +53,14 @@ def test_struct_layouts_match_header(tmp_path):
 int main(void) {
   F(skv_config, n_layers) F(skv_config, n_q_heads) F(skv_config, n_kv_heads) F(skv_config, head_dim)
   F(skv_config, tokens_per_frame) F(skv_config, capacity) F(skv_config, max_frames) F(skv_config, dtype)
-  F(skv_config, softmax_scale) F(skv_config, pos_offset) F(skv_config, policy) F(skv_config, reserved)
+  F(skv_config, softmax_scale) F(skv_config, pos_offset) F(skv_config, policy) F(skv_config, max_decode_tokens)
   F(skv_state_view_t, k) F(skv_state_view_t, v) F(skv_state_view_t, pos) F(skv_state_view_t, score)
   F(skv_state_view_t, size) F(skv_state_view_t, capacity) F(skv_state_view_t, frame)
   F(skv_state_view_t, pool_score) F(skv_state_view_t, pool_pos) F(skv_state_view_t, pool_size)
   F(skv_state_view_t, pool_stride)
   F(skv_cache_view_t, k) F(skv_cache_view_t, v) F(skv_cache_view_t, n_tokens) F(skv_cache_view_t, max_tokens)
-  F(skv_cache_view_t, n_kv_heads) F(skv_cache_view_t, head_dim)
+  F(skv_cache_view_t, n_kv_heads) F(skv_cache_view_t, head_dim) F(skv_cache_view_t, decode_row0)
+  F(skv_cache_view_t, decode_tokens)
   printf("sizeof.skv_config %zu\nsizeof.skv_state_view_t %zu\nsizeof.skv_cache_view_t %zu\n",
          sizeof(skv_config), sizeof(skv_state_view_t), sizeof(skv_cache_view_t));
   return 0;
@@ -97,7 +98,7 @@ def _cfg(**kw):
     (dict(pos_offset=-3), B.SKV_ERR_INVALID_ARG),
     (dict(policy=3), B.SKV_ERR_INVALID_ARG),
     (dict(policy=-1), B.SKV_ERR_INVALID_ARG),
-    (dict(reserved=1), B.SKV_ERR_INVALID_ARG),
+    (dict(max_decode_tokens=-1), B.SKV_ERR_INVALID_ARG),
 ])
 def test_init_rejects_bad_configs_before_touching_the_device(lib, kw, status):
     h = ctypes.c_void_p(123)
@@ -112,6 +113,7 @@ def test_null_arguments(lib):
     assert lib.skv_init(None, None, ctypes.byref(h)) == B.SKV_ERR_INVALID_ARG
     assert lib.skv_init(ctypes.byref(_cfg()), None, None) == B.SKV_ERR_INVALID_ARG
     assert lib.skv_frame_step(None, 0, 1, None, None, None, None) == B.SKV_ERR_INVALID_ARG
+    assert lib.skv_decode_step(None, 0, 1, 1, None, None, None, None) == B.SKV_ERR_INVALID_ARG
     assert lib.skv_state_view(None, 0, None) == B.SKV_ERR_INVALID_ARG
     assert lib.skv_decode_cache_view(None, 0, None) == B.SKV_ERR_INVALID_ARG
     assert lib.skv_reset(None) == B.SKV_ERR_INVALID_ARG
