@@ -142,6 +142,46 @@ def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
     return res
 
 
+def decode_bench(wl, q_all, k_all, v_all, out, stream, n_calls=32):
+    """Decoding after a whole video: one token per call over the detailed cache D of every
+    layer (all T * N video tokens), the step the paper runs after prefill.  HBM-bound: each
+    call reads all of D's K and V once."""
+    from paper_2605_31598_amd import FrameStepper
+    import torch
+
+    N, T, L = wl.n_frames, wl.tokens_per_frame, wl.n_layers
+    st = FrameStepper.from_workload(wl, stream=stream, max_decode_tokens=n_calls + 8)
+    try:
+        for f in range(N):
+            st.step(q_all[f], k_all[f], v_all[f], out)
+        g = torch.Generator(device="cuda").manual_seed(wl.seed + 1)
+        q = torch.randn((n_calls + 8, L, wl.n_q_heads, 1, wl.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        k = torch.randn((n_calls + 8, L, wl.n_kv_heads, 1, wl.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        v = torch.randn((n_calls + 8, L, wl.n_kv_heads, 1, wl.head_dim), generator=g, device="cuda").to(torch.bfloat16)
+        o = torch.empty((L, wl.n_q_heads, 1, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+        for i in range(8):  # warm-up calls
+            st.decode(q[i], k[i], v[i], o)
+        torch.cuda.synchronize()
+        st.timing_start(n_calls)
+        t0 = time.perf_counter()
+        for i in range(8, 8 + n_calls):
+            st.decode(q[i], k[i], v[i], o)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms = st.timing_stop(n_calls).astype(np.float64)
+    finally:
+        st.close()
+    keys = N * T + 8 + np.arange(n_calls) + 1  # keys per query of each timed call
+    kv_bytes = keys * L * wl.n_kv_heads * wl.head_dim * 2 * 2  # K and V of every key, read once
+    att = ms[:, 0]
+    gbs = float(kv_bytes.sum() / (att.sum() * 1e-3) / 1e9)
+    return {"kernel": "decode_split_kernel<128> + decode_combine_kernel<128>", "tokens_per_call": 1,
+            "cached_tokens_per_kv_head": int(N * T), "calls": n_calls,
+            "ms_per_call": round(float(att.mean()), 4), "tokens_per_s": round(n_calls / wall, 1),
+            "kv_bytes_per_call": float(kv_bytes.mean()), "GBps": round(gbs, 1), "peak_GBps": PEAK_HBM_GBS,
+            "frac": round(gbs / PEAK_HBM_GBS, 4), "append_ms_per_call": round(float(ms[:, 1].mean()), 4)}
+
+
 def cpu_baseline(wl, seconds):
     """The fp64 oracle on a bounded sample: layer 0, frames from state-full onward, on a
     full state of the most recent tokens; scaled to frames/s of the whole stack."""
@@ -335,6 +375,7 @@ def main():
     }
     if not args.no_baselines:
         result["baselines"] = baselines(wl, q_all, k_all, v_all, out, stream, med)
+        result["decode"] = decode_bench(wl, q_all, k_all, v_all, out, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)

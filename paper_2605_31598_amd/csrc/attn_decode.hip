@@ -213,15 +213,18 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   if (r >= a.G * a.t) return;  // no barriers below
   const size_t item0 = static_cast<size_t>(blk) * a.n_split;
   const float c = a.scale_log2;
+  const float* ml = a.part_ml + item0 * 64 + row;
   float mx = -1e30f;
-  for (int sp = 0; sp < a.n_split; ++sp) mx = fmaxf(mx, a.part_ml[(item0 + sp) * 64 + row]);
+#pragma unroll 4
+  for (int sp = 0; sp < a.n_split; ++sp) mx = fmaxf(mx, ml[static_cast<size_t>(sp) * 64]);
   float acc[DPT];
 #pragma unroll
   for (int i = 0; i < DPT; ++i) acc[i] = 0.f;
   float lsum = 0.f;
+#pragma unroll 4
   for (int sp = 0; sp < a.n_split; ++sp) {
-    const float w = fast_exp2((a.part_ml[(item0 + sp) * 64 + row] - mx) * c);
-    lsum += a.part_ml[(item0 + sp) * 64 + 32 + row] * w;
+    const float w = fast_exp2((ml[static_cast<size_t>(sp) * 64] - mx) * c);
+    lsum += ml[static_cast<size_t>(sp) * 64 + 32] * w;
     const float* po = a.part_o + (item0 + sp) * 32 * D + static_cast<size_t>(row) * D + dq * DPT;
 #pragma unroll
     for (int i = 0; i < DPT; i += 4) {

@@ -79,7 +79,8 @@ struct DecodeArgs {
 };
 
 constexpr int kDecodeMaxTokens = 64;  // new tokens per decode call
-constexpr int kDecodeItems = 8192;    // split items aimed at per call (partials sized for it)
+constexpr int kDecodeItems = 2048;    // split items aimed at per call: one wave per SIMD slot of the
+                                      // 256-CU device at two waves per SIMD (partials sized for it)
 
 constexpr int kMfmaRowsPerWave = 32;    // query rows (G*T packed) per attention wave
 constexpr int kMfmaWaves = 8;           // waves per attention workgroup (at most)
