@@ -85,6 +85,58 @@ class StepResult:
     kept: np.ndarray  # [H_kv, min(B, S+T)] indices into the pool, ascending position
     state: LayerState  # C_n
     flops: int  # multiply-add work of the attention, 4*d per visible (query, key) pair per head
+    k_stored: np.ndarray | None = None  # the frame's keys as C and D store them (rotated with RoPE)
+
+
+# ----------------------------------------------------------------------------
+# Rotary position embedding at virtual positions
+# ----------------------------------------------------------------------------
+@dataclass
+class RopeSpec:
+    """RoPE applied to Q and K inside the step (virtual sequence length and RoPE scaling
+    paragraphs): pair frequencies f_j (j < d/2), the cos/sin multiplier, and the dtype
+    the rotated activations are rounded to ("bf16" or "f32", as the model stores them)."""
+
+    freqs: np.ndarray
+    mscale: float
+    dtype: str
+
+
+def rope_spec(head_dim, theta, kind="plain", factor=1.0, orig_max=0, dtype="bf16") -> RopeSpec:
+    """f_j = theta^(-2j/d) (RoPE).  "yarn": YaRN's NTK-by-parts blend with scale s and original
+    context L: r_j = L f_j / (2 pi), g_j = clamp((r_j - 1) / (32 - 1), 0, 1),
+    f'_j = (1 - g_j) f_j / s + g_j f_j, and the temperature factor 0.1 ln(s) + 1 on cos/sin."""
+    j = np.arange(head_dim // 2, dtype=np.float64)
+    f = theta ** (-2.0 * j / head_dim)
+    if kind == "plain":
+        return RopeSpec(f, 1.0, dtype)
+    if kind != "yarn":
+        raise ValueError(kind)
+    r = orig_max * f / (2.0 * np.pi)
+    g = np.clip((r - 1.0) / (32.0 - 1.0), 0.0, 1.0)
+    return RopeSpec((1.0 - g) * f / factor + g * f, 0.1 * np.log(factor) + 1.0, dtype)
+
+
+def round_to_dtype(x, dtype):
+    """Round fp64 values to the nearest bf16 (ties to even) or fp32 value."""
+    if dtype == "f32":
+        return x.astype(np.float32).astype(np.float64)
+    # bf16: nearest multiple of 2^(e-7) for x in [2^e, 2^(e+1)); ties to an even mantissa
+    m, e = np.frexp(x)  # x = m 2^e, 0.5 <= |m| < 1
+    scaled = np.ldexp(m, 8)  # 8 significant bits
+    return np.ldexp(np.round(scaled), e - 8)  # np.round: half to even
+
+
+def rope_rotate(x, positions, spec: RopeSpec):
+    """x [..., P, d] at positions [P]: half-split pairs (j, j + d/2) rotated by p f_j, in fp64,
+    then rounded to the spec's dtype."""
+    h = x.shape[-1] // 2
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * spec.freqs[None, :]
+    c = np.cos(ang) * spec.mscale
+    s = np.sin(ang) * spec.mscale
+    lo, hi = x[..., :h], x[..., h:]
+    out = np.concatenate([lo * c - hi * s, hi * c + lo * s], axis=-1)
+    return round_to_dtype(out, spec.dtype)
 
 
 # ----------------------------------------------------------------------------
@@ -166,13 +218,15 @@ POLICIES = ("statekv", "recent", "full")
 
 
 def frame_step(state: LayerState, q, k, v, frame, capacity, scale=None, pos_offset=0,
-               keep_attn=False, policy="statekv") -> StepResult:
+               keep_attn=False, policy="statekv", rope: RopeSpec | None = None) -> StepResult:
     """One layer of one frame: attention over [C_{n-1}; frame], scores, refresh.
 
     q [H_q, T, d], k/v [H_kv, T, d] as float64 (exact widened input values).
     ``policy`` picks the refresh: "statekv" (Top-B by score, Eq. 6), "recent" (the B
     most recent candidates) or "full" (keep every candidate; ``capacity`` ignored, so
-    the state is the whole token history and the step is streaming full attention)."""
+    the state is the whole token history and the step is streaming full attention).
+    With ``rope``, Q and K are rotated at the frame's virtual positions first, and the
+    rotated keys are what the state keeps (the state's keys are already rotated)."""
     if policy not in POLICIES:
         raise ValueError(f"unknown policy {policy!r}")
     H_q, T, d = q.shape
@@ -181,6 +235,9 @@ def frame_step(state: LayerState, q, k, v, frame, capacity, scale=None, pos_offs
         scale = 1.0 / np.sqrt(d)
     S = state.size
     fpos = frame_positions(frame, T, pos_offset)
+    if rope is not None:
+        q = rope_rotate(q, fpos, rope)
+        k = rope_rotate(k, fpos, rope)
     k_pool = np.concatenate([state.k, k], axis=1)
     v_pool = np.concatenate([state.v, v], axis=1)
     pool_pos = np.concatenate([state.pos, np.broadcast_to(fpos, (H_kv, T))], axis=1)
@@ -214,7 +271,7 @@ def frame_step(state: LayerState, q, k, v, frame, capacity, scale=None, pos_offs
         score=scores[rows, kept].copy(),
     )
     flops = int(visibility(S, T).sum()) * H_q * 4 * d
-    return StepResult(out, attn, pool_pos, scores, kept, new_state, flops)
+    return StepResult(out, attn, pool_pos, scores, kept, new_state, flops, k)
 
 
 @dataclass
@@ -237,7 +294,7 @@ class DecodeCache:
 
 
 def run_layer(inputs, n_frames, capacity, n_kv_heads, head_dim, scale=None, pos_offset=0,
-              state=None, start_frame=0, callback=None, policy="statekv"):
+              state=None, start_frame=0, callback=None, policy="statekv", rope=None):
     """Stream ``n_frames`` frames of one layer.  ``inputs(frame)`` returns float64
     (q, k, v).  Returns (final state, decode cache, list of StepResult)."""
     st = state.copy() if state is not None else LayerState.empty(n_kv_heads, head_dim)
@@ -245,20 +302,25 @@ def run_layer(inputs, n_frames, capacity, n_kv_heads, head_dim, scale=None, pos_
     results = []
     for n in range(start_frame, start_frame + n_frames):
         q, k, v = inputs(n)
-        r = frame_step(st, q, k, v, n, capacity, scale, pos_offset, policy=policy)
-        cache.append(k, v)  # D_n = D_{n-1} with the frame's K/V appended
+        r = frame_step(st, q, k, v, n, capacity, scale, pos_offset, policy=policy, rope=rope)
+        cache.append(r.k_stored, v)  # D_n = D_{n-1} with the frame's K/V appended
         st = r.state
         results.append(r if callback is None else callback(n, r))
     return st, cache, results
 
 
-def decode_attention(q, k_hist, v_hist, k_new, v_new, scale=None):
+def decode_attention(q, k_hist, v_hist, k_new, v_new, scale=None, rope: RopeSpec | None = None, positions=None):
     """Decoding after (or between) frames reads the detailed state D, not C (the decoding
     paragraph): the t new tokens attend to every earlier token of D (the video's tokens, then
     the tokens decoded before), all visible, and to the new tokens up to themselves (causal).
     That is Eq. 5 with the whole history as the memory.
 
-    q [H_q, t, d]; k_hist, v_hist [H_kv, n, d]; k_new, v_new [H_kv, t, d].  Returns [H_q, t, d]."""
+    q [H_q, t, d]; k_hist, v_hist [H_kv, n, d] (keys as D stores them); k_new, v_new
+    [H_kv, t, d].  With ``rope``, the new tokens' Q and K are rotated at ``positions`` [t]
+    first.  Returns [H_q, t, d]."""
+    if rope is not None:
+        q = rope_rotate(q, positions, rope)
+        k_new = rope_rotate(k_new, positions, rope)
     H_q, t, d = q.shape
     H_kv = k_new.shape[0]
     if scale is None:

@@ -187,6 +187,57 @@ def check_decode_is_causal_sdpa(seed=8, H_q=6, H_kv=2, d=8, T=4, N=3, chunks=(1,
         pos += t
 
 
+def check_rope_closed_form():
+    """d = 4, theta = 100: pair frequencies 1 and 1/10; unit vectors rotate in the planes
+    (0, 2) and (1, 3) by p and p/10, counter-clockwise, and keep their norm."""
+    spec = orc.rope_spec(4, 100.0, dtype="f32")
+    p = np.array([0.0, 1.0, 7.0, 1234.0])
+    e0 = np.broadcast_to(np.array([1.0, 0.0, 0.0, 0.0]), (4, 4))
+    e1 = np.broadcast_to(np.array([0.0, 1.0, 0.0, 0.0]), (4, 4))
+    e3 = np.broadcast_to(np.array([0.0, 0.0, 0.0, 1.0]), (4, 4))
+    np.testing.assert_allclose(orc.rope_rotate(e0, p, spec), np.stack([np.cos(p), 0 * p, np.sin(p), 0 * p], 1),
+                               atol=1e-7)
+    np.testing.assert_allclose(orc.rope_rotate(e1, p, spec),
+                               np.stack([0 * p, np.cos(p / 10), 0 * p, np.sin(p / 10)], 1), atol=1e-7)
+    np.testing.assert_allclose(orc.rope_rotate(e3, p, spec),
+                               np.stack([0 * p, -np.sin(p / 10), 0 * p, np.cos(p / 10)], 1), atol=1e-7)
+
+
+def check_rope_relative_positions(seed=10, H_q=4, H_kv=2, d=8, T=4, N=4, B=6):
+    """RoPE logits depend only on position differences, so shifting the whole stream's
+    virtual positions (pos_offset) changes neither outputs nor scores (fp32-rounded
+    rotations: to rounding), while the stored positions shift."""
+    video = random_video(seed, H_q, H_kv, d, T, N)
+    spec = orc.rope_spec(d, 10000.0, dtype="f32")
+    runs = []
+    for off in (0, 100000):
+        st = orc.LayerState.empty(H_kv, d)
+        res = []
+        for n, (q, k, v) in enumerate(video):
+            r = orc.frame_step(st, q, k, v, n, B, d ** -0.5, off, rope=spec)
+            st = r.state
+            res.append(r)
+        runs.append(res)
+    for a, b in zip(*runs):
+        np.testing.assert_allclose(a.out, b.out, atol=2e-5)
+        np.testing.assert_allclose(a.pool_score, b.pool_score, rtol=1e-4)
+        assert np.array_equal(a.pool_pos + 100000, b.pool_pos)
+
+
+def check_yarn_limits():
+    """YaRN with s = 1 is plain RoPE; with s > 1 the highest frequency (r >> 32) is kept,
+    the lowest (r < 1) is divided by s, and cos/sin carry 0.1 ln(s) + 1."""
+    plain = orc.rope_spec(128, 1e4)
+    same = orc.rope_spec(128, 1e4, "yarn", factor=1.0, orig_max=4096)
+    np.testing.assert_allclose(same.freqs, plain.freqs, rtol=1e-15, atol=0)
+    assert same.mscale == 1.0
+    y = orc.rope_spec(128, 1e4, "yarn", factor=8.0, orig_max=4096)
+    assert y.freqs[0] == plain.freqs[0]
+    np.testing.assert_allclose(y.freqs[-1], plain.freqs[-1] / 8.0, rtol=1e-15)
+    assert abs(y.mscale - (0.1 * math.log(8.0) + 1.0)) < 1e-15
+    assert np.all(np.diff(y.freqs) < 0) and np.all(y.freqs <= plain.freqs)
+
+
 def check_zero_query_closed_form(H_q=6, H_kv=3, d=4, T=5, N=6, B=7):
     G = H_q // H_kv
     rng = np.random.default_rng(3)
@@ -236,6 +287,21 @@ def test_recent_policy_keeps_the_last_tokens():
 def test_decode_over_the_detailed_cache_equals_causal_sdpa():
     check_decode_is_causal_sdpa()
     check_decode_is_causal_sdpa(seed=9, H_q=7, H_kv=1, d=16, T=5, N=2, chunks=(4, 2))
+
+
+def test_rope_closed_form_and_relative_positions():
+    check_rope_closed_form()
+    check_rope_relative_positions()
+
+
+def test_yarn_reduces_to_rope_and_blends_by_wavelength():
+    check_yarn_limits()
+
+
+def test_rope_bf16_rounding_matches_a_library_conversion():
+    x = np.random.default_rng(3).standard_normal(4096) * 10.0 ** np.random.default_rng(4).uniform(-3, 3, 4096)
+    ref = torch.from_numpy(x).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(orc.round_to_dtype(x, "bf16"), ref)
 
 
 def test_golden_handworked():
@@ -420,6 +486,23 @@ def _mut_positions_physical(frame, T, pos_offset=0):
     return pos_offset + np.arange(T, dtype=np.int64) + frame  # wrong: not from the virtual length
 
 
+def _mut_rope_interleaved(x, positions, spec):
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * spec.freqs[None, :]
+    c, s_ = np.cos(ang) * spec.mscale, np.sin(ang) * spec.mscale
+    ev, od = x[..., 0::2], x[..., 1::2]  # wrong: adjacent pairs instead of (j, j + d/2)
+    out = np.empty_like(x)
+    out[..., 0::2] = ev * c - od * s_
+    out[..., 1::2] = od * c + ev * s_
+    return orc.round_to_dtype(out, spec.dtype)
+
+
+_ROPE = orc.rope_rotate
+
+
+def _mut_rope_clockwise(x, positions, spec):
+    return _ROPE(x, -np.asarray(positions, dtype=np.float64), spec)  # wrong direction
+
+
 def _mut_recent_oldest(pos, capacity):
     P = pos.shape[0]
     keep = np.arange(P) if P <= capacity else np.argsort(pos, kind="stable")[:capacity]  # wrong: oldest
@@ -430,7 +513,8 @@ PINS = [check_golden, check_full_capacity_is_causal_sdpa,
         lambda: check_full_capacity_is_causal_sdpa(seed=11, H_q=14, H_kv=2, d=16, T=7, N=3),
         check_zero_capacity_is_framewise_sdpa, check_zero_query_closed_form,
         lambda: check_bruteforce(1, 4, 2, 4, 4, 3, 4, 5), check_full_policy_is_causal_sdpa,
-        check_recent_policy_window, check_decode_is_causal_sdpa]
+        check_recent_policy_window, check_decode_is_causal_sdpa, check_rope_closed_form,
+        check_rope_relative_positions]
 
 
 @pytest.mark.parametrize("name,attr,mutant", [
@@ -443,6 +527,8 @@ PINS = [check_golden, check_full_capacity_is_causal_sdpa,
     ("keeps the lowest scores", "select_top", _mut_select_lowest),
     ("positions from physical length", "frame_positions", _mut_positions_physical),
     ("recency window keeps the oldest", "select_recent", _mut_recent_oldest),
+    ("RoPE pairs adjacent dimensions", "rope_rotate", _mut_rope_interleaved),
+    ("RoPE rotates clockwise", "rope_rotate", _mut_rope_clockwise),
 ])
 def test_planted_mistake_is_caught(monkeypatch, name, attr, mutant):
     monkeypatch.setattr(orc, attr, mutant)
