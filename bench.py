@@ -102,14 +102,18 @@ def full_attention_flops(wl, n):
 def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
     """The paper's two comparison systems on the same resident inputs, outside the timed
     region of the main line: streaming full attention over the decode cache (one whole
-    video, per-frame times) and the recency window of B tokens (one video)."""
+    video, per-frame times) and the recency window of B tokens (one video); and StateKV
+    with YaRN-scaled RoPE applied inside the step at virtual positions (one video)."""
     from paper_2605_31598_amd import FrameStepper
     import torch
 
     N, T = wl.n_frames, wl.tokens_per_frame
     res = {}
-    for policy in ("full", "recent"):
-        st = FrameStepper.from_workload(wl, stream=stream, policy=policy)
+    runs = {"full": dict(policy="full"), "recent": dict(policy="recent"),
+            "statekv_yarn": dict(policy="statekv", rope="yarn", rope_theta=1e6, rope_factor=4.0, rope_orig_max=32768)}
+    for name, kw in runs.items():
+        policy = kw["policy"]
+        st = FrameStepper.from_workload(wl, stream=stream, **kw)
         try:
             for f in range(4):  # warm the kernels, then restart the stream
                 st.step(q_all[f], k_all[f], v_all[f], out)
@@ -136,8 +140,8 @@ def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
             slower = np.nonzero(frame_ms > statekv_ms)[0]
             entry["crossover_frame"] = int(slower[0]) if slower.size else None
             entry["statekv_speedup_at_last_frame"] = round(float(frame_ms[-1] / statekv_ms), 2)
-        res[policy] = entry
-        print(f"[bench] {policy}: {entry['frames_per_s']} frames/s over one video", file=sys.stderr, flush=True)
+        res[name] = entry
+        print(f"[bench] {name}: {entry['frames_per_s']} frames/s over one video", file=sys.stderr, flush=True)
     res["statekv_frame_ms_state_full"] = round(statekv_ms, 4)
     return res
 

@@ -63,6 +63,25 @@ typedef enum { SKV_BF16 = 0, SKV_F32 = 1 } skv_dtype;
  *                       empty. */
 typedef enum { SKV_POLICY_STATEKV = 0, SKV_POLICY_RECENT = 1, SKV_POLICY_FULL = 2 } skv_policy;
 
+/* Rotary position embedding applied inside the step (virtual sequence length
+ * paragraph: positions come from L_n, not from the cache size; RoPE scaling
+ * paragraph: one scaling for cache building and decoding).  With SKV_ROPE_NONE
+ * the inputs are used as given.  Otherwise the library rotates Q and K of every
+ * frame (and of every decoded token) at their virtual positions
+ * p = pos_offset + n*T + t (decoded tokens continue after the frames done),
+ * and the compressed state and the decode cache hold the rotated keys.
+ * Pairing is half-split: dimension j < d/2 rotates with j + d/2 by the angle
+ * p * f_j, f_j = rope_theta^(-2j/d):
+ *   x'_j = x_j cos - x_{j+d/2} sin,   x'_{j+d/2} = x_{j+d/2} cos + x_j sin.
+ * SKV_ROPE_YARN uses YaRN's frequencies and temperature with scale s =
+ * rope_factor and original context rope_orig_max: per dimension, r_j =
+ * rope_orig_max * f_j / (2 pi), g_j = clamp((r_j - 1) / (32 - 1), 0, 1),
+ * f'_j = (1 - g_j) f_j / s + g_j f_j, and cos and sin are multiplied by
+ * 0.1 ln(s) + 1.  Angles are reduced in double precision on the host (a
+ * table of cos/sin per position); rotated values are rounded to the config
+ * dtype. */
+typedef enum { SKV_ROPE_NONE = 0, SKV_ROPE_PLAIN = 1, SKV_ROPE_YARN = 2 } skv_rope;
+
 /* Problem statement of the method: head counts and head dimension d_h (Eq. 5),
  * T tokens per frame, capacity B of the compressed state (Eq. 4), layer count,
  * and the decode-cache length, which grows by T per frame. */
@@ -79,6 +98,10 @@ typedef struct {
   int64_t pos_offset;       /* virtual position of the first video token (room for a text prefix) */
   int32_t policy;           /* skv_policy; 0 (a zeroed config) is StateKV */
   int32_t max_decode_tokens; /* rows of D kept for tokens decoded after the video (>= 0) */
+  int32_t rope;             /* skv_rope; 0 (a zeroed config): no rotation */
+  float rope_theta;         /* RoPE base (> 0 when rope != 0), e.g. 10000 or 1e6 */
+  float rope_factor;        /* YaRN scale s >= 1 (SKV_ROPE_YARN only) */
+  int32_t rope_orig_max;    /* YaRN original context length (> 0, SKV_ROPE_YARN only) */
 } skv_config;
 
 typedef struct skv_ctx skv_ctx;

@@ -30,6 +30,10 @@ SKV_POLICY_STATEKV = 0
 SKV_POLICY_RECENT = 1
 SKV_POLICY_FULL = 2
 POLICIES = {"statekv": SKV_POLICY_STATEKV, "recent": SKV_POLICY_RECENT, "full": SKV_POLICY_FULL}
+
+SKV_ROPE_NONE = 0
+SKV_ROPE_PLAIN = 1
+SKV_ROPE_YARN = 2
 N_STAGES = 2
 STAGES = ("attention", "refresh")
 
@@ -46,6 +50,8 @@ class skv_config(ctypes.Structure):
         ("head_dim", ctypes.c_int32), ("tokens_per_frame", ctypes.c_int32), ("capacity", ctypes.c_int32),
         ("max_frames", ctypes.c_int32), ("dtype", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
         ("pos_offset", ctypes.c_int64), ("policy", ctypes.c_int32), ("max_decode_tokens", ctypes.c_int32),
+        ("rope", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("rope_factor", ctypes.c_float),
+        ("rope_orig_max", ctypes.c_int32),
     ]
 
 

@@ -86,6 +86,15 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_kernel(DecodeArgs
     if (row_valid) x = *reinterpret_cast<const u32x4*>(qg + static_cast<size_t>(r) * D + ks * 16 + h * 8);
     qreg[ks] = __builtin_bit_cast(bf16x8, x);
   }
+  if (a.rope_tab != nullptr && row_valid) {  // RoPE at the decoded token's virtual position
+    const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + r % a.t) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS / 2; ++ks) {
+      const u32x4 lo = __builtin_bit_cast(u32x4, qreg[ks]), hi = __builtin_bit_cast(u32x4, qreg[ks + KS / 2]);
+      qreg[ks] = __builtin_bit_cast(bf16x8, rope_chunk_bf16(lo, hi, false, ks * 16 + h * 8, tb));
+      qreg[ks + KS / 2] = __builtin_bit_cast(bf16x8, rope_chunk_bf16(hi, lo, true, ks * 16 + h * 8, tb));
+    }
+  }
 
   // global -> registers for one 32-key block starting at key kb
   u32x4 kreg[KS], vreg[VIT];
@@ -98,6 +107,16 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_kernel(DecodeArgs
       u32x4 x = {0u, 0u, 0u, 0u};
       if (kin) x = *reinterpret_cast<const u32x4*>(kr + ks * 16 + h * 8);
       kreg[ks] = x;
+    }
+    const int jn = jk - a.S - a.n_dec;  // new token (not yet in D, so not yet rotated)
+    if (a.rope_tab != nullptr && kin && jn >= 0) {
+      const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + jn) * D;
+#pragma unroll
+      for (int ks = 0; ks < KS / 2; ++ks) {
+        const u32x4 lo = kreg[ks], hi = kreg[ks + KS / 2];
+        kreg[ks] = rope_chunk_bf16(lo, hi, false, ks * 16 + h * 8, tb);
+        kreg[ks + KS / 2] = rope_chunk_bf16(hi, lo, true, ks * 16 + h * 8, tb);
+      }
     }
   };
   auto load_v = [&](int kb) {

@@ -104,6 +104,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_full_kernel(AttnArgs a) {
     if (row_valid) x = *reinterpret_cast<const u32x4*>(qg + static_cast<size_t>(r_lane) * D + ks * 16 + h * 8);
     qreg[ks] = __builtin_bit_cast(bf16x8, x);
   }
+  if (a.rope_tab != nullptr && row_valid) {  // RoPE at the frame token's virtual position
+    const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + r_lane % a.T) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS / 2; ++ks) {
+      const u32x4 lo = __builtin_bit_cast(u32x4, qreg[ks]), hi = __builtin_bit_cast(u32x4, qreg[ks + KS / 2]);
+      qreg[ks] = __builtin_bit_cast(bf16x8, rope_chunk_bf16(lo, hi, false, ks * 16 + h * 8, tb));
+      qreg[ks + KS / 2] = __builtin_bit_cast(bf16x8, rope_chunk_bf16(hi, lo, true, ks * 16 + h * 8, tb));
+    }
+  }
 
   // ---------------- staging (global -> registers -> LDS) ----------------
   u32x4 kpre[ITEMS], vpre[ITEMS];
@@ -123,6 +132,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_full_kernel(AttnArgs a) {
       }
       kpre[it] = x;
       vpre[it] = y;
+    }
+    // RoPE of the frame's keys (cached and state keys are stored rotated): the
+    // other half of a key row's chunk ch is chunk ch ^ KCH/2, held by lane ^ KCH/2
+    if (a.rope_tab != nullptr && (t + 1) * kKT > S) {
+#pragma unroll
+      for (int it = 0; it < ITEMS; ++it) {
+        const int idx = it * kThreads + tid;
+        const int kk = idx / KCH, ch = idx % KCH;
+        const int j = t * kKT + kk;
+        u32x4 other;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) other[w] = static_cast<unsigned>(__shfl_xor(static_cast<int>(kpre[it][w]), KCH / 2, 64));
+        if (j >= S && j < n_keys) {
+          const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + (j - S)) * D;
+          kpre[it] = rope_chunk_bf16(kpre[it], other, ch >= KCH / 2, (ch % (KCH / 2)) * 8, tb);
+        }
+      }
     }
   };
   auto store_tile = [&](int b) {

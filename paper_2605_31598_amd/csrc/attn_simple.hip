@@ -34,6 +34,14 @@ __device__ inline void store_elem<uint16_t>(uint16_t* p, float x) {
   *p = static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);  // round to nearest even
 }
 
+// A value as the storage type holds it (rotated activations are rounded to it).
+template <typename T>
+__device__ inline float round_storage(float x);
+template <>
+__device__ inline float round_storage<float>(float x) { return x; }
+template <>
+__device__ inline float round_storage<uint16_t>(float x) { return static_cast<float>(static_cast<__bf16>(x)); }
+
 constexpr int KT = 32;  // keys per LDS tile
 
 }  // namespace
@@ -65,6 +73,14 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
 
   float q[D];
   for (int e = 0; e < D; ++e) q[e] = valid ? load_elem(qrow + e) : 0.f;
+  if (a.rope_tab != nullptr && valid) {  // RoPE at the frame token's virtual position
+    const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + r % a.T) * D;
+    for (int j = 0; j < D / 2; ++j) {
+      const float lo = q[j], hi = q[j + D / 2], c = tb[2 * j], s = tb[2 * j + 1];
+      q[j] = round_storage<T>(rope_first(lo, hi, c, s));
+      q[j + D / 2] = round_storage<T>(rope_second(hi, lo, c, s));
+    }
+  }
 
   auto stage = [&](int t0, bool with_v) {
     for (int idx = tid; idx < KT * D; idx += 64) {
@@ -77,6 +93,12 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
       } else if (j < n_keys) {
         kx = load_elem(kfr + static_cast<size_t>(j - S) * D + e);
         if (with_v) vx = load_elem(vfr + static_cast<size_t>(j - S) * D + e);
+        if (a.rope_tab != nullptr) {  // the frame's keys are rotated here; earlier keys are stored rotated
+          const int jj = e % (D / 2);
+          const float other = load_elem(kfr + static_cast<size_t>(j - S) * D + (e < D / 2 ? e + D / 2 : e - D / 2));
+          const float* tb = a.rope_tab + (static_cast<size_t>(a.rope_pos0 + (j - S)) * D) + 2 * jj;
+          kx = round_storage<T>(e < D / 2 ? rope_first(kx, other, tb[0], tb[1]) : rope_second(kx, other, tb[0], tb[1]));
+        }
       }
       ks[kk][e] = kx;
       if (with_v) vs[kk][e] = vx;

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "plan.h"
+#include "rope.h"
 
 namespace skv {
 
@@ -26,6 +27,8 @@ struct AttnArgs {
   int kv_rows;
   int tile_stride, pool_stride;
   float scale_log2;    // softmax scale * log2(e)
+  const float* rope_tab;  // null: no rotation; else {cos, sin} per (relative position, pair)
+  int rope_pos0;          // relative position of frame token 0 (n * T)
 };
 
 // The refresh launch finishes a frame for `n_layers` layers: score finalisation,
@@ -53,6 +56,9 @@ struct RefreshArgs {
   int32_t frame_pos0;        // virtual position of frame token 0
   float inv_T;
   int mode;                  // 0: Top-B by score, 1: the B most recent, 2: append only
+  const float* rope_tab;     // null: copy keys as given; else rotate them (frame token t at rope_pos0 + t)
+  int rope_pos0;
+  int elem;                  // bytes per value: 2 (bf16) or 4 (fp32)
 };
 
 // Decode over the detailed cache (split-key flash decoding).  Each wave of the
@@ -76,6 +82,8 @@ struct DecodeArgs {
   int split;           // keys per split, a multiple of 32
   int n_split;         // ceil((S + n_dec + t) / split)
   float scale_log2;
+  const float* rope_tab;  // null: no rotation; else new token i sits at relative position rope_pos0 + i
+  int rope_pos0;
 };
 
 constexpr int kDecodeMaxTokens = 64;  // new tokens per decode call

@@ -165,6 +165,29 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// Rotated copy of the two 16-byte chunks c and c + chunks/2 of one key row
+// (RoPE pairs are half-split, so chunk c of the lower half pairs with the same
+// chunk of the upper half); pos = the row's relative position.
+__device__ inline void copy_key_pair(const char* src, char* dst, int c, int chunks, int elem, int pos,
+                                     const float* tab) {
+  const int d = chunks * 16 / elem;
+  const int half = chunks / 2;
+  const u32x4 lo = *reinterpret_cast<const u32x4*>(src + c * 16);
+  const u32x4 hi = *reinterpret_cast<const u32x4*>(src + (c + half) * 16);
+  const float* tb = tab + static_cast<size_t>(pos) * d;
+  const int j0 = c * 16 / elem;
+  u32x4 a, b;
+  if (elem == 2) {
+    a = rope_chunk_bf16(lo, hi, false, j0, tb);
+    b = rope_chunk_bf16(hi, lo, true, j0, tb);
+  } else {
+    a = rope_chunk_f32(lo, hi, false, j0, tb);
+    b = rope_chunk_f32(hi, lo, true, j0, tb);
+  }
+  *reinterpret_cast<u32x4*>(dst + c * 16) = a;
+  *reinterpret_cast<u32x4*>(dst + (c + half) * 16) = b;
+}
+
 __device__ inline void copy16(const void* src, void* dst, size_t off) {
   *reinterpret_cast<u32x4*>(static_cast<char*>(dst) + off) =
       *reinterpret_cast<const u32x4*>(static_cast<const char*>(src) + off);
@@ -260,8 +283,14 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
     const int src = asrc[i], dst = adst[i];
     const size_t so = src_base + static_cast<size_t>(src) * a.row_bytes + (static_cast<size_t>(c) << 4);
     const size_t dof = dst_base + static_cast<size_t>(dst) * a.row_bytes + (static_cast<size_t>(c) << 4);
-    *reinterpret_cast<u32x4*>(static_cast<char*>(a.ks) + dof) =
-        *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.kf) + so);
+    if (a.rope_tab == nullptr) {
+      *reinterpret_cast<u32x4*>(static_cast<char*>(a.ks) + dof) =
+          *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.kf) + so);
+    } else if (c < chunks / 2) {  // the frame's keys are stored rotated
+      copy_key_pair(static_cast<const char*>(a.kf) + src_base + static_cast<size_t>(src) * a.row_bytes,
+                    static_cast<char*>(a.ks) + dst_base + static_cast<size_t>(dst) * a.row_bytes, c, chunks, a.elem,
+                    a.rope_pos0 + src, a.rope_tab);
+    }
     *reinterpret_cast<u32x4*>(static_cast<char*>(a.vs) + dof) =
         *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.vf) + so);
     if (c == 0) {
@@ -280,9 +309,18 @@ __device__ void append_frame(const RefreshArgs& a, int lg) {
   const char* vf = static_cast<const char*>(a.vf) + src;
   char* ck = static_cast<char*>(a.ck) + dst;
   char* cv = static_cast<char*>(a.cv) + dst;
+  const int chunks = a.row_bytes >> 4;
   for (size_t off = static_cast<size_t>(threadIdx.x) << 4; off < bytes; off += static_cast<size_t>(blockDim.x) << 4) {
-    copy16(kf, ck, off);
     copy16(vf, cv, off);
+    if (a.rope_tab == nullptr) {
+      copy16(kf, ck, off);
+    } else {  // keys are stored rotated; token r of the block sits at rope_pos0 + r
+      const int r = static_cast<int>(off / a.row_bytes);
+      const int c = static_cast<int>((off % a.row_bytes) >> 4);
+      if (c < chunks / 2)
+        copy_key_pair(kf + static_cast<size_t>(r) * a.row_bytes, ck + static_cast<size_t>(r) * a.row_bytes, c, chunks,
+                      a.elem, a.rope_pos0 + r, a.rope_tab);
+    }
   }
 }
 

@@ -69,6 +69,7 @@ struct skv_ctx {
   int32_t* pool_pos = nullptr;
   int32_t* admit_src = nullptr;    // [L][H_kv][T]
   int32_t* admit_dst = nullptr;
+  float* rope_tab = nullptr;       // RoPE {cos, sin} per (relative position, pair), or null
   float* dec_part_o = nullptr;     // decode split partials: [dec_items][32][d]
   float* dec_part_ml = nullptr;    // [dec_items][2][32]
   int dec_items = 0;
@@ -124,6 +125,44 @@ int layer_frames_done(const skv_ctx* c, int layer) {
 int state_size(const skv_ctx* c, int64_t frames_done) {
   const int64_t seen = frames_done * c->cfg.tokens_per_frame;
   return static_cast<int>(seen < c->cfg.capacity ? seen : c->cfg.capacity);
+}
+
+// RoPE table: for relative position p (virtual position pos_offset + p) and pair
+// j < d/2, {cos, sin} of (pos_offset + p) * f_j times the YaRN temperature, in
+// double precision (exact range reduction of large angles), rounded to fp32.
+skv_status build_rope_table(skv_ctx* c) {
+  const skv_config& cfg = c->cfg;
+  if (cfg.rope == SKV_ROPE_NONE) return SKV_OK;
+  const int d = cfg.head_dim, half = d / 2;
+  std::vector<double> f(static_cast<size_t>(half));
+  double mscale = 1.0;
+  for (int j = 0; j < half; ++j) f[j] = std::pow(static_cast<double>(cfg.rope_theta), -2.0 * j / d);
+  if (cfg.rope == SKV_ROPE_YARN) {
+    const double s = cfg.rope_factor, two_pi = 6.283185307179586476925286766559;
+    for (int j = 0; j < half; ++j) {
+      const double r = cfg.rope_orig_max * f[j] / two_pi;
+      const double g = std::min(1.0, std::max(0.0, (r - 1.0) / (32.0 - 1.0)));
+      f[j] = (1.0 - g) * f[j] / s + g * f[j];
+    }
+    mscale = 0.1 * std::log(s) + 1.0;
+  }
+  const size_t n_pos = static_cast<size_t>(c->max_tokens);
+  std::vector<float> tab(n_pos * d);
+  for (size_t p = 0; p < n_pos; ++p) {
+    const double pos = static_cast<double>(cfg.pos_offset + static_cast<int64_t>(p));
+    for (int j = 0; j < half; ++j) {
+      const double ang = pos * f[j];
+      tab[p * d + 2 * j] = static_cast<float>(std::cos(ang) * mscale);
+      tab[p * d + 2 * j + 1] = static_cast<float>(std::sin(ang) * mscale);
+    }
+  }
+  void* dev = nullptr;
+  const skv_status s = alloc(c, tab.size() * sizeof(float), &dev);
+  if (s != SKV_OK) return s;
+  const hipError_t e = hipMemcpy(dev, tab.data(), tab.size() * sizeof(float), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy of the RoPE table");
+  c->rope_tab = static_cast<float*>(dev);
+  return SKV_OK;
 }
 
 // Uploads the attention work plan of every layer_count (1 .. n_layers).  The
@@ -207,6 +246,12 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
     return fail(SKV_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0");
   if (c.pos_offset < 0) return fail(SKV_ERR_INVALID_ARG, "pos_offset must be >= 0");
   if (c.max_decode_tokens < 0) return fail(SKV_ERR_INVALID_ARG, "max_decode_tokens must be >= 0");
+  if (c.rope != SKV_ROPE_NONE && c.rope != SKV_ROPE_PLAIN && c.rope != SKV_ROPE_YARN)
+    return fail(SKV_ERR_INVALID_ARG, "unknown rope kind");
+  if (c.rope != SKV_ROPE_NONE && !(c.rope_theta > 0.f && std::isfinite(c.rope_theta)))
+    return fail(SKV_ERR_INVALID_ARG, "rope_theta must be finite and > 0");
+  if (c.rope == SKV_ROPE_YARN && (!(c.rope_factor >= 1.f && std::isfinite(c.rope_factor)) || c.rope_orig_max < 1))
+    return fail(SKV_ERR_INVALID_ARG, "YaRN needs rope_factor >= 1 and rope_orig_max >= 1");
   const int64_t video_tokens = static_cast<int64_t>(c.max_frames) * c.tokens_per_frame;
   const int64_t max_tokens = video_tokens + c.max_decode_tokens;
   if (c.pos_offset + max_tokens >= (int64_t{1} << 31)) return fail(SKV_ERR_INVALID_ARG, "positions exceed int32");
@@ -287,7 +332,8 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
       return hip_fail(e, "hipMemsetAsync");
     }
   }
-  const skv_status ps = build_plans(ctx, static_cast<int>(rows));
+  skv_status ps = build_plans(ctx, static_cast<int>(rows));
+  if (ps == SKV_OK) ps = build_rope_table(ctx);
   if (ps != SKV_OK) {
     release(ctx);
     delete ctx;
@@ -339,6 +385,8 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.partial = full ? nullptr : ctx->partial + lh0 * ctx->tile_stride * ctx->pool_stride;
   aa.work = plan.work;
   aa.n_work = plan.n_work;
+  aa.rope_tab = ctx->rope_tab;
+  aa.rope_pos0 = static_cast<int>(ctx->frame * T);
   aa.n_layers = layer_count;
   aa.H_q = c.n_q_heads;
   aa.H_kv = Hkv;
@@ -378,6 +426,9 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.frame_pos0 = pos0;
   ra.inv_T = 1.0f / static_cast<float>(T);
   ra.mode = c.policy == SKV_POLICY_STATEKV ? 0 : (c.policy == SKV_POLICY_RECENT ? 1 : 2);
+  ra.rope_tab = ctx->rope_tab;
+  ra.rope_pos0 = static_cast<int>(ctx->frame * T);
+  ra.elem = ctx->elem;
 
   hipError_t e = mark(0);
   if (e == hipSuccess)
@@ -451,6 +502,8 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   da.split = split;
   da.n_split = (n_keys + split - 1) / split;
   da.scale_log2 = ctx->scale_log2;
+  da.rope_tab = ctx->rope_tab;
+  da.rope_pos0 = S + n_dec;
 
   // append of the new tokens' K/V to D's decode rows (the refresh kernel's append-only mode)
   skv::RefreshArgs ra{};
@@ -465,6 +518,9 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   ra.T = t;
   ra.row_bytes = static_cast<int>(rb);
   ra.mode = 2;
+  ra.rope_tab = ctx->rope_tab;
+  ra.rope_pos0 = S + n_dec;
+  ra.elem = ctx->elem;
 
   const bool timing = ctx->timing_n < ctx->timing_max;
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;

@@ -19,7 +19,7 @@ class FrameStepper:
 
     def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
                  dtype="bf16", softmax_scale=0.0, pos_offset=0, stream=None, policy="statekv",
-                 max_decode_tokens=0):
+                 max_decode_tokens=0, rope=None, rope_theta=0.0, rope_factor=1.0, rope_orig_max=0):
         import torch
 
         if not torch.cuda.is_available():
@@ -32,16 +32,18 @@ class FrameStepper:
         self.elem = 2 if dtype == "bf16" else 4
         self.policy = policy
         self.cfg = B.skv_config(n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
-                                _DTYPES[dtype], softmax_scale, pos_offset, B.POLICIES[policy], max_decode_tokens)
+                                _DTYPES[dtype], softmax_scale, pos_offset, B.POLICIES[policy], max_decode_tokens,
+                                {None: B.SKV_ROPE_NONE, "plain": B.SKV_ROPE_PLAIN, "yarn": B.SKV_ROPE_YARN}[rope],
+                                rope_theta, rope_factor, rope_orig_max)
         self.n_layers, self.H_q, self.H_kv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         # streaming full attention keeps no compressed state
         self.T, self.B, self.max_frames = tokens_per_frame, (0 if policy == "full" else capacity), max_frames
         self.ctx = B.skv_init(self.cfg, self.stream.cuda_stream)
 
     @classmethod
-    def from_workload(cls, wl, max_frames=None, stream=None, policy="statekv", max_decode_tokens=0):
+    def from_workload(cls, wl, max_frames=None, stream=None, policy="statekv", max_decode_tokens=0, **rope):
         return cls(wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.tokens_per_frame, wl.capacity,
-                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream, policy, max_decode_tokens)
+                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream, policy, max_decode_tokens, **rope)
 
     # ------------------------------------------------------------------ step
     def _check(self, name, t, heads, n_layers):
