@@ -113,7 +113,9 @@ __device__ inline float column_reduce(const float (&cs)[16], int lane) {
 
 }  // namespace
 
-template <int D>
+// ROPE: rotate Q and the frame's keys at their virtual positions (a separate
+// instantiation, so the kernel without rotation carries none of its code).
+template <int D, bool ROPE>
 __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = D / 16;                   // k-steps of K Q^T
   constexpr int DB = D / 32;                   // 32-column blocks of O
@@ -160,7 +162,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (row_valid) x = *reinterpret_cast<const u32x4*>(qg + static_cast<size_t>(r_lane) * D + ks * 16 + h * 8);
     qreg[ks] = __builtin_bit_cast(bf16x8, x);
   }
-  if (a.rope_tab != nullptr && row_valid) {  // RoPE at the frame token's virtual position
+  if (ROPE && row_valid) {  // RoPE at the frame token's virtual position
     const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + r_lane % a.T) * D;
 #pragma unroll
     for (int ks = 0; ks < KS / 2; ++ks) {
@@ -191,7 +193,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     }
     // RoPE of the frame's keys (cached and state keys are stored rotated): the
     // other half of a key row's chunk ch is chunk ch ^ KCH/2, held by lane ^ KCH/2
-    if (a.rope_tab != nullptr && (t + 1) * kKT > S) {
+    if (ROPE && (t + 1) * kKT > S) {
 #pragma unroll
       for (int it = 0; it < ITEMS; ++it) {
         const int idx = it * kThreads + tid;
@@ -396,20 +398,35 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
 
 hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
   const int grid = a.n_work;
+  const bool rope = a.rope_tab != nullptr;
   if (head_dim == 128) {
-    hipLaunchKernelGGL(attn_mfma_kernel<128>, dim3(grid), dim3(kThreads), sizeof(Smem<128>), s, a);
+    if (rope)
+      hipLaunchKernelGGL((attn_mfma_kernel<128, true>), dim3(grid), dim3(kThreads), sizeof(Smem<128>), s, a);
+    else
+      hipLaunchKernelGGL((attn_mfma_kernel<128, false>), dim3(grid), dim3(kThreads), sizeof(Smem<128>), s, a);
   } else {
-    hipLaunchKernelGGL(attn_mfma_kernel<64>, dim3(grid), dim3(kThreads), sizeof(Smem<64>), s, a);
+    if (rope)
+      hipLaunchKernelGGL((attn_mfma_kernel<64, true>), dim3(grid), dim3(kThreads), sizeof(Smem<64>), s, a);
+    else
+      hipLaunchKernelGGL((attn_mfma_kernel<64, false>), dim3(grid), dim3(kThreads), sizeof(Smem<64>), s, a);
   }
   return hipGetLastError();
 }
 
 hipError_t prepare_attention_mfma() {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(attn_mfma_kernel<128>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<128>));
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(attn_mfma_kernel<64>),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<64>));
+  const void* kernels[] = {reinterpret_cast<const void*>(attn_mfma_kernel<128, false>),
+                            reinterpret_cast<const void*>(attn_mfma_kernel<128, true>)};
+  for (const void* k : kernels) {
+    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<128>));
+    if (e != hipSuccess) return e;
+  }
+  const void* kernels64[] = {reinterpret_cast<const void*>(attn_mfma_kernel<64, false>),
+                              reinterpret_cast<const void*>(attn_mfma_kernel<64, true>)};
+  for (const void* k : kernels64) {
+    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<64>));
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace skv
