@@ -146,6 +146,40 @@ def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
     return res
 
 
+def diagnostics_bench(stream, n_frames=32, budgets=(16, 256, 1024)):
+    """The appendix's assumption diagnostics on a synthetic stream of the one-layer 7B shape,
+    keeping every token so each frame's scores cover its whole history.  On i.i.d. inputs
+    they describe the generator, not a video model: reported for completeness."""
+    from paper_2605_31598_amd import FrameStepper
+    from paper_2605_31598_amd import diagnostics as dg
+    from workloads import CONFIGS
+    from workloads import device as wdev
+    from workloads import generate as gen
+    import torch
+
+    wl = CONFIGS["vlm7b_1layer"]
+    wl = wl.with_(capacity=n_frames * wl.tokens_per_frame, n_frames=n_frames)
+    T, d = wl.tokens_per_frame, wl.head_dim
+    st = FrameStepper.from_workload(wl, stream=stream)
+    q = torch.empty((n_frames, 1, wl.n_q_heads, T, d), dtype=torch.bfloat16, device="cuda")
+    k = torch.empty((n_frames, 1, wl.n_kv_heads, T, d), dtype=torch.bfloat16, device="cuda")
+    v = torch.empty_like(k)
+    for t, tid in ((q, gen.TENSOR_Q), (k, gen.TENSOR_K), (v, gen.TENSOR_V)):
+        wdev.fill_iid(t, [gen.stream_key(wl.seed, 0, f, tid) for f in range(n_frames)], "bf16")
+    out = torch.empty((1, wl.n_q_heads, T, d), dtype=torch.bfloat16, device="cuda")
+    frames = []
+    try:
+        for n in range(n_frames):
+            st.step(q[n], k[n], v[n], out)
+            s, p = dg.layer_frames_from_stepper(st, 0, T)
+            frames.append((s, p, wl.pos_offset + n * T))
+    finally:
+        st.close()
+    res = dg.summarise(frames, list(budgets))
+    return {"stream": f"{wl.name}, {n_frames} frames, i.i.d. inputs", **{str(b): {k2: round(v2, 4) for k2, v2 in r.items()}
+                                                                       for b, r in res.items()}}
+
+
 def decode_bench(wl, q_all, k_all, v_all, out, stream, n_calls=32):
     """Decoding after a whole video: one token per call over the detailed cache D of every
     layer (all T * N video tokens), the step the paper runs after prefill.  HBM-bound: each
@@ -380,6 +414,7 @@ def main():
     if not args.no_baselines:
         result["baselines"] = baselines(wl, q_all, k_all, v_all, out, stream, med)
         result["decode"] = decode_bench(wl, q_all, k_all, v_all, out, stream)
+        result["diagnostics"] = diagnostics_bench(stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
