@@ -207,15 +207,41 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
   int32_t* asrc = a.admit_src + static_cast<size_t>(lg) * T;
   int32_t* adst = a.admit_dst + static_cast<size_t>(lg) * T;
 
-  for (int j = tid; j < P; j += blockDim.x) {
-    float acc = 0.f;
-    for (int t = 0; t < n_tiles; ++t) acc += part[static_cast<size_t>(t) * a.pool_stride + j];
-    const float s = acc * a.inv_T;
-    const int32_t pos = j < S ? state_pos[j] : a.frame_pos0 + (j - S);
-    pscore[j] = s;
-    ppos[j] = pos;
-    sbits[j] = __float_as_uint(s);
-    spos[j] = pos;
+  // Each thread sums up to kJ candidates at a time, loading kTB row tiles of
+  // each before adding them, so the loads overlap instead of waiting one by one;
+  // the tiles are still added in order 0, 1, ... (padding adds exact zeros).
+  constexpr int kJ = 4, kTB = 8;
+  for (int j0 = tid; j0 < P; j0 += kJ * static_cast<int>(blockDim.x)) {
+    float acc[kJ];
+#pragma unroll
+    for (int q = 0; q < kJ; ++q) acc[q] = 0.f;
+    for (int t0 = 0; t0 < n_tiles; t0 += kTB) {
+      float v[kJ][kTB];
+#pragma unroll
+      for (int q = 0; q < kJ; ++q)
+#pragma unroll
+        for (int u = 0; u < kTB; ++u) {
+          const int j = min(j0 + q * static_cast<int>(blockDim.x), P - 1);
+          const int t = min(t0 + u, n_tiles - 1);
+          v[q][u] = part[static_cast<size_t>(t) * a.pool_stride + j];
+        }
+#pragma unroll
+      for (int q = 0; q < kJ; ++q)
+#pragma unroll
+        for (int u = 0; u < kTB; ++u) acc[q] += t0 + u < n_tiles ? v[q][u] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < kJ; ++q) {
+      const int j = j0 + q * static_cast<int>(blockDim.x);
+      if (j < P) {
+        const float s = acc[q] * a.inv_T;
+        const int32_t pos = j < S ? state_pos[j] : a.frame_pos0 + (j - S);
+        pscore[j] = s;
+        ppos[j] = pos;
+        sbits[j] = __float_as_uint(s);
+        spos[j] = pos;
+      }
+    }
   }
   __syncthreads();
 
@@ -301,25 +327,45 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
 }
 
 // Decode-cache append of one (layer, KV head): T contiguous rows of K and V.
+// Four 16-byte chunks per thread are loaded before any is stored.
 __device__ void append_frame(const RefreshArgs& a, int lg) {
-  const size_t bytes = static_cast<size_t>(a.T) * a.row_bytes;
-  const size_t src = static_cast<size_t>(lg) * bytes;
-  const size_t dst = (static_cast<size_t>(lg) * a.max_tokens + a.first_row) * a.row_bytes;
+  const int rb = a.row_bytes;
+  const int chunks = rb >> 4;
+  const int n16 = a.T * chunks;  // 16-byte chunks of the block
+  const size_t src = static_cast<size_t>(lg) * a.T * rb;
+  const size_t dst = (static_cast<size_t>(lg) * a.max_tokens + a.first_row) * rb;
   const char* kf = static_cast<const char*>(a.kf) + src;
   const char* vf = static_cast<const char*>(a.vf) + src;
   char* ck = static_cast<char*>(a.ck) + dst;
   char* cv = static_cast<char*>(a.cv) + dst;
-  const int chunks = a.row_bytes >> 4;
-  for (size_t off = static_cast<size_t>(threadIdx.x) << 4; off < bytes; off += static_cast<size_t>(blockDim.x) << 4) {
-    copy16(vf, cv, off);
-    if (a.rope_tab == nullptr) {
-      copy16(kf, ck, off);
-    } else {  // keys are stored rotated; token r of the block sits at rope_pos0 + r
-      const int r = static_cast<int>(off / a.row_bytes);
-      const int c = static_cast<int>((off % a.row_bytes) >> 4);
-      if (c < chunks / 2)
-        copy_key_pair(kf + static_cast<size_t>(r) * a.row_bytes, ck + static_cast<size_t>(r) * a.row_bytes, c, chunks,
-                      a.elem, a.rope_pos0 + r, a.rope_tab);
+  const int nt = static_cast<int>(blockDim.x);
+  constexpr int kU = 4;
+  for (int base = threadIdx.x; base < n16; base += kU * nt) {
+    u32x4 vv[kU], kv[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const size_t off = static_cast<size_t>(min(base + u * nt, n16 - 1)) << 4;
+      vv[u] = *reinterpret_cast<const u32x4*>(vf + off);
+      if (a.rope_tab == nullptr) kv[u] = *reinterpret_cast<const u32x4*>(kf + off);
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int i = base + u * nt;
+      if (i < n16) {
+        const size_t off = static_cast<size_t>(i) << 4;
+        *reinterpret_cast<u32x4*>(cv + off) = vv[u];
+        if (a.rope_tab == nullptr) *reinterpret_cast<u32x4*>(ck + off) = kv[u];
+      }
+    }
+  }
+  if (a.rope_tab != nullptr) {
+    // keys are stored rotated; token r of the block sits at rope_pos0 + r, and
+    // chunk c of the lower half pairs with chunk c of the upper half
+    const int half = chunks / 2;
+    for (int p = threadIdx.x; p < a.T * half; p += nt) {
+      const int r = p / half, c = p - r * half;
+      copy_key_pair(kf + static_cast<size_t>(r) * rb, ck + static_cast<size_t>(r) * rb, c, chunks, a.elem,
+                    a.rope_pos0 + r, a.rope_tab);
     }
   }
 }
