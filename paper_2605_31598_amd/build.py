@@ -18,7 +18,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = ["statekv.hip", "attn_mfma.hip", "attn_full.hip", "attn_decode.hip", "attn_simple.hip", "refresh.hip", "plan.cpp"]
+SOURCES = ["statekv.hip", "attn_mfma.hip", "attn_full.hip", "attn_decode.hip", "attn_simple.hip", "refresh.hip",
+           "rope_keys.hip", "plan.cpp"]
 LIB = os.path.join(PKG, "libstatekv.so")
 GEN_SRC = os.path.join(ROOT, "workloads", "csrc", "skv_gen.hip")
 GEN_LIB = os.path.join(ROOT, "workloads", "libskvgen.so")

@@ -108,16 +108,6 @@ __global__ __launch_bounds__(kDecThreads, 2) void decode_split_kernel(DecodeArgs
       if (kin) x = *reinterpret_cast<const u32x4*>(kr + ks * 16 + h * 8);
       kreg[ks] = x;
     }
-    const int jn = jk - a.S - a.n_dec;  // new token (not yet in D, so not yet rotated)
-    if (a.rope_tab != nullptr && kin && jn >= 0) {
-      const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + jn) * D;
-#pragma unroll
-      for (int ks = 0; ks < KS / 2; ++ks) {
-        const u32x4 lo = kreg[ks], hi = kreg[ks + KS / 2];
-        kreg[ks] = rope_chunk_bf16(lo, hi, false, ks * 16 + h * 8, tb);
-        kreg[ks + KS / 2] = rope_chunk_bf16(hi, lo, true, ks * 16 + h * 8, tb);
-      }
-    }
   };
   auto load_v = [&](int kb) {
 #pragma unroll

@@ -60,8 +60,9 @@ __device__ inline unsigned pack_bf16x2(float lo, float hi) {
 
 }  // namespace
 
-// ROPE: rotate Q and the frame's keys at their virtual positions (a separate
-// instantiation, so the kernel without rotation carries none of its code).
+// ROPE: rotate Q at the frame tokens' virtual positions (a separate
+// instantiation, so the kernel without rotation carries none of its code).  The
+// frame's keys arrive rotated (rope_keys.hip), like the state's and the cache's.
 template <int D, bool ROPE>
 __global__ __launch_bounds__(kThreads, 1) void attn_full_kernel(AttnArgs a) {
   constexpr int KS = D / 16;                   // k-steps of K Q^T
@@ -134,23 +135,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_full_kernel(AttnArgs a) {
       }
       kpre[it] = x;
       vpre[it] = y;
-    }
-    // RoPE of the frame's keys (cached and state keys are stored rotated): the
-    // other half of a key row's chunk ch is chunk ch ^ KCH/2, held by lane ^ KCH/2
-    if (ROPE && (t + 1) * kKT > S) {
-#pragma unroll
-      for (int it = 0; it < ITEMS; ++it) {
-        const int idx = it * kThreads + tid;
-        const int kk = idx / KCH, ch = idx % KCH;
-        const int j = t * kKT + kk;
-        u32x4 other;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) other[w] = static_cast<unsigned>(__shfl_xor(static_cast<int>(kpre[it][w]), KCH / 2, 64));
-        if (j >= S && j < n_keys) {
-          const float* tb = a.rope_tab + static_cast<size_t>(a.rope_pos0 + (j - S)) * D;
-          kpre[it] = rope_chunk_bf16(kpre[it], other, ch >= KCH / 2, (ch % (KCH / 2)) * 8, tb);
-        }
-      }
     }
   };
   auto store_tile = [&](int b) {

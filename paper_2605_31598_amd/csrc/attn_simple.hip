@@ -93,12 +93,6 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
       } else if (j < n_keys) {
         kx = load_elem(kfr + static_cast<size_t>(j - S) * D + e);
         if (with_v) vx = load_elem(vfr + static_cast<size_t>(j - S) * D + e);
-        if (a.rope_tab != nullptr) {  // the frame's keys are rotated here; earlier keys are stored rotated
-          const int jj = e % (D / 2);
-          const float other = load_elem(kfr + static_cast<size_t>(j - S) * D + (e < D / 2 ? e + D / 2 : e - D / 2));
-          const float* tb = a.rope_tab + (static_cast<size_t>(a.rope_pos0 + (j - S)) * D) + 2 * jj;
-          kx = round_storage<T>(e < D / 2 ? rope_first(kx, other, tb[0], tb[1]) : rope_second(kx, other, tb[0], tb[1]));
-        }
       }
       ks[kk][e] = kx;
       if (with_v) vs[kk][e] = vx;

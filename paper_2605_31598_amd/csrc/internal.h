@@ -27,7 +27,8 @@ struct AttnArgs {
   int kv_rows;
   int tile_stride, pool_stride;
   float scale_log2;    // softmax scale * log2(e)
-  const float* rope_tab;  // null: no rotation; else {cos, sin} per (relative position, pair)
+  const float* rope_tab;  // null: no rotation; else rotate Q by {cos, sin} per (relative position,
+                          // pair); kf holds the frame's keys already rotated
   int rope_pos0;          // relative position of frame token 0 (n * T)
 };
 
@@ -56,9 +57,6 @@ struct RefreshArgs {
   int32_t frame_pos0;        // virtual position of frame token 0
   float inv_T;
   int mode;                  // 0: Top-B by score, 1: the B most recent, 2: append only
-  const float* rope_tab;     // null: copy keys as given; else rotate them (frame token t at rope_pos0 + t)
-  int rope_pos0;
-  int elem;                  // bytes per value: 2 (bf16) or 4 (fp32)
 };
 
 // Decode over the detailed cache (split-key flash decoding).  Each wave of the
@@ -82,8 +80,8 @@ struct DecodeArgs {
   int split;           // keys per split, a multiple of 32
   int n_split;         // ceil((S + n_dec + t) / split)
   float scale_log2;
-  const float* rope_tab;  // null: no rotation; else new token i sits at relative position rope_pos0 + i
-  int rope_pos0;
+  const float* rope_tab;  // null: no rotation; else rotate Q (new token i at relative position
+  int rope_pos0;          // rope_pos0 + i); kn holds the new keys already rotated
 };
 
 constexpr int kDecodeMaxTokens = 64;  // new tokens per decode call
@@ -101,6 +99,10 @@ hipError_t launch_attention_full_bf16(const AttnArgs& a, int head_dim, hipStream
 hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s);
 hipError_t launch_decode_bf16(const DecodeArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s);
+// Rotates n_blocks * t key rows (t rows per (layer, KV head) block, row r at
+// relative position pos0 + r) from `in` to `out`; same layout, either dtype.
+hipError_t launch_rope_keys(const void* in, void* out, int n_blocks, int t, int row_bytes, int elem,
+                            const float* tab, int pos0, hipStream_t s);
 hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride);
 
 }  // namespace skv

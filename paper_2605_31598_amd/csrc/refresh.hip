@@ -165,29 +165,6 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Rotated copy of the two 16-byte chunks c and c + chunks/2 of one key row
-// (RoPE pairs are half-split, so chunk c of the lower half pairs with the same
-// chunk of the upper half); pos = the row's relative position.
-__device__ inline void copy_key_pair(const char* src, char* dst, int c, int chunks, int elem, int pos,
-                                     const float* tab) {
-  const int d = chunks * 16 / elem;
-  const int half = chunks / 2;
-  const u32x4 lo = *reinterpret_cast<const u32x4*>(src + c * 16);
-  const u32x4 hi = *reinterpret_cast<const u32x4*>(src + (c + half) * 16);
-  const float* tb = tab + static_cast<size_t>(pos) * d;
-  const int j0 = c * 16 / elem;
-  u32x4 a, b;
-  if (elem == 2) {
-    a = rope_chunk_bf16(lo, hi, false, j0, tb);
-    b = rope_chunk_bf16(hi, lo, true, j0, tb);
-  } else {
-    a = rope_chunk_f32(lo, hi, false, j0, tb);
-    b = rope_chunk_f32(hi, lo, true, j0, tb);
-  }
-  *reinterpret_cast<u32x4*>(dst + c * 16) = a;
-  *reinterpret_cast<u32x4*>(dst + (c + half) * 16) = b;
-}
-
 __device__ inline void copy16(const void* src, void* dst, size_t off) {
   *reinterpret_cast<u32x4*>(static_cast<char*>(dst) + off) =
       *reinterpret_cast<const u32x4*>(static_cast<const char*>(src) + off);
@@ -309,14 +286,8 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
     const int src = asrc[i], dst = adst[i];
     const size_t so = src_base + static_cast<size_t>(src) * a.row_bytes + (static_cast<size_t>(c) << 4);
     const size_t dof = dst_base + static_cast<size_t>(dst) * a.row_bytes + (static_cast<size_t>(c) << 4);
-    if (a.rope_tab == nullptr) {
-      *reinterpret_cast<u32x4*>(static_cast<char*>(a.ks) + dof) =
-          *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.kf) + so);
-    } else if (c < chunks / 2) {  // the frame's keys are stored rotated
-      copy_key_pair(static_cast<const char*>(a.kf) + src_base + static_cast<size_t>(src) * a.row_bytes,
-                    static_cast<char*>(a.ks) + dst_base + static_cast<size_t>(dst) * a.row_bytes, c, chunks, a.elem,
-                    a.rope_pos0 + src, a.rope_tab);
-    }
+    *reinterpret_cast<u32x4*>(static_cast<char*>(a.ks) + dof) =
+        *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.kf) + so);
     *reinterpret_cast<u32x4*>(static_cast<char*>(a.vs) + dof) =
         *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.vf) + so);
     if (c == 0) {
@@ -330,8 +301,7 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
 // Four 16-byte chunks per thread are loaded before any is stored.
 __device__ void append_frame(const RefreshArgs& a, int lg) {
   const int rb = a.row_bytes;
-  const int chunks = rb >> 4;
-  const int n16 = a.T * chunks;  // 16-byte chunks of the block
+  const int n16 = a.T * (rb >> 4);  // 16-byte chunks of the block
   const size_t src = static_cast<size_t>(lg) * a.T * rb;
   const size_t dst = (static_cast<size_t>(lg) * a.max_tokens + a.first_row) * rb;
   const char* kf = static_cast<const char*>(a.kf) + src;
@@ -346,7 +316,7 @@ __device__ void append_frame(const RefreshArgs& a, int lg) {
     for (int u = 0; u < kU; ++u) {
       const size_t off = static_cast<size_t>(min(base + u * nt, n16 - 1)) << 4;
       vv[u] = *reinterpret_cast<const u32x4*>(vf + off);
-      if (a.rope_tab == nullptr) kv[u] = *reinterpret_cast<const u32x4*>(kf + off);
+      kv[u] = *reinterpret_cast<const u32x4*>(kf + off);
     }
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
@@ -354,18 +324,8 @@ __device__ void append_frame(const RefreshArgs& a, int lg) {
       if (i < n16) {
         const size_t off = static_cast<size_t>(i) << 4;
         *reinterpret_cast<u32x4*>(cv + off) = vv[u];
-        if (a.rope_tab == nullptr) *reinterpret_cast<u32x4*>(ck + off) = kv[u];
+        *reinterpret_cast<u32x4*>(ck + off) = kv[u];
       }
-    }
-  }
-  if (a.rope_tab != nullptr) {
-    // keys are stored rotated; token r of the block sits at rope_pos0 + r, and
-    // chunk c of the lower half pairs with chunk c of the upper half
-    const int half = chunks / 2;
-    for (int p = threadIdx.x; p < a.T * half; p += nt) {
-      const int r = p / half, c = p - r * half;
-      copy_key_pair(kf + static_cast<size_t>(r) * rb, ck + static_cast<size_t>(r) * rb, c, chunks, a.elem,
-                    a.rope_pos0 + r, a.rope_tab);
     }
   }
 }

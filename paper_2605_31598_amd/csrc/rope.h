@@ -1,6 +1,6 @@
-// Rotary position embedding at virtual positions, shared by every kernel that
-// rotates queries or keys, so that the attention kernels and the copies into the
-// compressed state and the decode cache produce bit-identical rotated keys.
+// Rotary position embedding at virtual positions, shared by the kernels that
+// rotate queries (the attention kernels, at load) and new keys (rope_keys.hip,
+// once per step), so that every rotation uses the same table and arithmetic.
 //
 // The host builds the table once per context: for relative position p (virtual
 // position minus pos_offset) and pair j < d/2, tab[(p * d/2 + j) * 2 + {0, 1}] =

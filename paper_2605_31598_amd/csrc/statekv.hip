@@ -70,6 +70,7 @@ struct skv_ctx {
   int32_t* admit_src = nullptr;    // [L][H_kv][T]
   int32_t* admit_dst = nullptr;
   float* rope_tab = nullptr;       // RoPE {cos, sin} per (relative position, pair), or null
+  void* rope_keys = nullptr;       // with RoPE: the step's new keys, rotated: [L][H_kv][new rows][d]
   float* dec_part_o = nullptr;     // decode split partials: [dec_items][32][d]
   float* dec_part_ml = nullptr;    // [dec_items][2][32]
   int dec_items = 0;
@@ -299,6 +300,9 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   }
 
   const size_t LH = static_cast<size_t>(c.n_layers) * c.n_kv_heads;
+  // rows of new keys per (layer, KV head) in one step: a frame, or one decode call
+  const int64_t new_rows =
+      std::max<int64_t>(c.tokens_per_frame, std::min<int64_t>(c.max_decode_tokens, skv::kDecodeMaxTokens));
   const size_t B_state = static_cast<size_t>(ctx->cfg.capacity);
   const size_t state_bytes = LH * B_state * ctx->row_bytes;
   const size_t cache_bytes = LH * static_cast<size_t>(max_tokens) * ctx->row_bytes;
@@ -315,6 +319,7 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
       {reinterpret_cast<void**>(&ctx->pool_pos), LH * ctx->pool_stride * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_src), LH * c.tokens_per_frame * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_dst), LH * c.tokens_per_frame * sizeof(int32_t)},
+      {&ctx->rope_keys, c.rope == SKV_ROPE_NONE ? 0 : LH * static_cast<size_t>(new_rows) * ctx->row_bytes},
       {reinterpret_cast<void**>(&ctx->dec_part_o), static_cast<size_t>(ctx->dec_items) * 32 * c.head_dim * sizeof(float)},
       {reinterpret_cast<void**>(&ctx->dec_part_ml), static_cast<size_t>(ctx->dec_items) * 64 * sizeof(float)},
   };
@@ -366,9 +371,12 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
   auto mark = [&](int i) -> hipError_t { return timing ? hipEventRecord(ev[i], ctx->stream) : hipSuccess; };
 
+  // with RoPE every later reader takes the frame's keys rotated (launched first below)
+  const void* k_used = ctx->rope_tab != nullptr ? ctx->rope_keys : k;
+
   skv::AttnArgs aa;
   aa.q = q;
-  aa.kf = k;
+  aa.kf = k_used;
   aa.vf = v;
   const bool full = c.policy == SKV_POLICY_FULL;
   if (full) {  // every earlier token, from the decode cache
@@ -403,7 +411,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.lg_tiles = plan.tiles;
   ra.tile_stride = ctx->tile_stride;
   ra.pool_stride = ctx->pool_stride;
-  ra.kf = k;
+  ra.kf = k_used;
   ra.vf = v;
   ra.ks = static_cast<char*>(ctx->state_k) + lh0 * B * rb;
   ra.vs = static_cast<char*>(ctx->state_v) + lh0 * B * rb;
@@ -426,11 +434,11 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.frame_pos0 = pos0;
   ra.inv_T = 1.0f / static_cast<float>(T);
   ra.mode = c.policy == SKV_POLICY_STATEKV ? 0 : (c.policy == SKV_POLICY_RECENT ? 1 : 2);
-  ra.rope_tab = ctx->rope_tab;
-  ra.rope_pos0 = static_cast<int>(ctx->frame * T);
-  ra.elem = ctx->elem;
 
   hipError_t e = mark(0);
+  if (e == hipSuccess && ctx->rope_tab != nullptr)
+    e = skv::launch_rope_keys(k, ctx->rope_keys, layer_count * Hkv, T, static_cast<int>(rb), ctx->elem, ctx->rope_tab,
+                              static_cast<int>(ctx->frame * T), ctx->stream);
   if (e == hipSuccess)
     e = !ctx->use_mfma ? skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream)
         : full         ? skv::launch_attention_full_bf16(aa, d, ctx->stream)
@@ -480,9 +488,12 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   const int per = std::max(1, ctx->dec_items / (LH * n_rb));  // splits per (layer-head, row block)
   const int split = std::max(256, ((n_keys + per - 1) / per + 31) / 32 * 32);
 
+  // with RoPE the kernels take the new tokens' keys rotated (launched first below)
+  const void* k_used = ctx->rope_tab != nullptr ? ctx->rope_keys : k;
+
   skv::DecodeArgs da;
   da.q = q;
-  da.kn = k;
+  da.kn = k_used;
   da.vn = v;
   da.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
   da.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
@@ -507,7 +518,7 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
 
   // append of the new tokens' K/V to D's decode rows (the refresh kernel's append-only mode)
   skv::RefreshArgs ra{};
-  ra.kf = k;
+  ra.kf = k_used;
   ra.vf = v;
   ra.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
   ra.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
@@ -518,14 +529,14 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   ra.T = t;
   ra.row_bytes = static_cast<int>(rb);
   ra.mode = 2;
-  ra.rope_tab = ctx->rope_tab;
-  ra.rope_pos0 = S + n_dec;
-  ra.elem = ctx->elem;
 
   const bool timing = ctx->timing_n < ctx->timing_max;
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
   auto mark = [&](int i) -> hipError_t { return timing ? hipEventRecord(ev[i], ctx->stream) : hipSuccess; };
   hipError_t e = mark(0);
+  if (e == hipSuccess && ctx->rope_tab != nullptr)
+    e = skv::launch_rope_keys(k, ctx->rope_keys, LH, t, static_cast<int>(rb), ctx->elem, ctx->rope_tab, S + n_dec,
+                              ctx->stream);
   if (e == hipSuccess) e = skv::launch_decode_bf16(da, d, ctx->stream);
   if (e == hipSuccess) e = mark(1);
   if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
