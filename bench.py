@@ -220,6 +220,63 @@ def decode_bench(wl, q_all, k_all, v_all, out, stream, n_calls=32):
             "frac": round(gbs / PEAK_HBM_GBS, 4), "append_ms_per_call": round(float(ms[:, 1].mean()), 4)}
 
 
+def large_bench(stream, name="vlm72b_80layer", timed=16):
+    """The 72B-shaped stack (80 layers, 64 Q / 8 KV heads, 256 tokens/frame, capacity 4096,
+    low-rank keys built on the device): the first frames fill the state, then `timed`
+    frames run at state full, all 80 layers per call.  Reported beside the 7B line."""
+    from paper_2605_31598_amd import FrameStepper
+    from workloads import CONFIGS
+    from workloads import device as wdev
+    from workloads import generate as gen
+    import torch
+
+    wl = CONFIGS[name]
+    L, Hq, Hkv, T, d = wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.tokens_per_frame, wl.head_dim
+    fill = -(-wl.capacity // T)  # frames until the state is full
+    F = fill + timed
+    q = torch.empty((F, L, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    k = torch.empty((F, L, Hkv, T, d), dtype=torch.bfloat16, device="cuda")
+    v = torch.empty_like(k)
+    for t, tid in ((q, gen.TENSOR_Q), (v, gen.TENSOR_V)):
+        wdev.fill_iid(t, [gen.stream_key(wl.seed, l, f, tid) for f in range(F) for l in range(L)], "bf16")
+    kl = torch.empty((F, Hkv, T, d), dtype=torch.bfloat16, device="cuda")
+    for l in range(L):
+        wdev.fill_lowrank_keys(kl, wl, l, range(F))
+        k[:, l].copy_(kl)
+    del kl
+    out = torch.empty((L, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    st = FrameStepper.from_workload(wl, max_frames=F, stream=stream)
+    try:
+        for n in range(fill):
+            st.step(q[n], k[n], v[n], out)
+        torch.cuda.synchronize()
+        st.timing_start(timed)
+        t0 = time.perf_counter()
+        for n in range(fill, F):
+            st.step(q[n], k[n], v[n], out)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        stages = st.timing_stop(timed).astype(np.float64)
+    finally:
+        st.close()
+    del q, k, v
+    att = stages[:, 0]
+    alg = attention_flops(wl, wl.capacity)
+    exe = executed_mfma_flops(wl, wl.capacity)
+    frame_ms = stages.sum(axis=1)
+    res = {"workload": name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "tokens_per_frame": T,
+           "capacity": wl.capacity, "inputs": "i.i.d. N(0,1) Q and V, low-rank keys (rank 16 + noise), bf16",
+           "timed_frames_at_state_full": timed, "frames_per_s": round(timed / wall, 2),
+           "ms_per_frame": round(1e3 * wall / timed, 4), "attention_ms": round(float(att.mean()), 4),
+           "refresh_ms": round(float(stages[:, 1].mean()), 4),
+           "attention_tflops": round(alg / (att.mean() * 1e-3) / 1e12, 1),
+           "attention_frac_of_bf16_peak": round(alg / (att.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "executed_mfma_frac": round(exe / (att.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "flatness_max_dev": round(float(np.max(np.abs(frame_ms / np.median(frame_ms) - 1.0))), 4)}
+    print(f"[bench] {name}: {res['frames_per_s']} frames/s at state full", file=sys.stderr, flush=True)
+    return res
+
+
 def cpu_baseline(wl, seconds):
     """The fp64 oracle on a bounded sample: layer 0, frames from state-full onward, on a
     full state of the most recent tokens; scaled to frames/s of the whole stack."""
@@ -274,7 +331,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-baselines", action="store_true",
-                    help="skip the Full SA and recency-window runs reported beside the main line")
+                    help="skip the runs reported beside the main line (Full SA, recency window, YaRN, decode, "
+                         "diagnostics, the 72B-shaped stack)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -415,6 +473,7 @@ def main():
         result["baselines"] = baselines(wl, q_all, k_all, v_all, out, stream, med)
         result["decode"] = decode_bench(wl, q_all, k_all, v_all, out, stream)
         result["diagnostics"] = diagnostics_bench(stream)
+        result["vlm72b"] = large_bench(stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -181,3 +181,18 @@ def test_device_generator_matches_host():
     t = CONFIGS["tiny_f32"]
     device.fill_iid(out32, [gen.stream_key(t.seed, 0, 5, gen.TENSOR_V)], "f32")
     assert np.array_equal(out32.cpu().numpy()[0], gen.frame_inputs(t, 0, 5)["v"].reshape(-1))
+
+
+def test_device_lowrank_keys_match_host():
+    """The 72B stack's low-rank keys, built on the device for the benchmark, equal the host generator's."""
+    from workloads import device
+
+    wl = CONFIGS["vlm72b_80layer"]
+    frames = [0, 9, 511]
+    for layer in (0, 41, 79):
+        out = torch.empty((len(frames), wl.n_kv_heads, wl.tokens_per_frame, wl.head_dim), dtype=torch.bfloat16,
+                          device="cuda")
+        device.fill_lowrank_keys(out, wl, layer, frames)
+        got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+        for i, f in enumerate(frames):
+            assert np.array_equal(got[i], gen.frame_inputs(wl, layer, f)["k"]), (layer, f)

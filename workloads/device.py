@@ -45,3 +45,29 @@ def fill_iid(out, keys, dtype: str, stream=None):
     if err != 0:
         raise RuntimeError(f"skvgen_fill failed: {err}")
     stream.synchronize()  # keeps the uploaded keys/table alive until the kernel has read them
+
+
+def fill_lowrank_keys(out, cfg, layer: int, frames, stream=None):
+    """Low-rank keys of one layer for ``frames``: ``out`` is a bf16 CUDA tensor
+    [len(frames), H_kv, T, d].  Bit-identical to ``generate.frame_inputs(...)["k"]``:
+    the same fp32 streams, the rank-one terms multiplied and added one at a time
+    (no fused multiply-add), then scaled and rounded to bf16 the same way."""
+    import torch
+
+    H, T, d, R = cfg.n_kv_heads, cfg.tokens_per_frame, cfg.head_dim, gen.LOWRANK_RANK
+    F = len(frames)
+    dev = out.device
+    W = torch.empty((1, H * R * d), dtype=torch.float32, device=dev)
+    fill_iid(W, [gen.stream_key(cfg.seed, layer, 0, gen.TENSOR_LOWRANK_W)], "f32", stream)
+    c = torch.empty((F, H * T * R), dtype=torch.float32, device=dev)
+    fill_iid(c, [gen.stream_key(cfg.seed, layer, f, gen.TENSOR_LOWRANK_C) for f in frames], "f32", stream)
+    eps = torch.empty((F, H * T * d), dtype=torch.float32, device=dev)
+    fill_iid(eps, [gen.stream_key(cfg.seed, layer, f, gen.TENSOR_K) for f in frames], "f32", stream)
+    W = W.view(H, R, d)
+    c = c.view(F, H, T, R)
+    acc = torch.zeros((F, H, T, d), dtype=torch.float32, device=dev)
+    for r in range(R):
+        prod = c[:, :, :, r:r + 1] * W[None, :, r, None, :]
+        acc = acc + prod
+    val = acc * 0.25 + eps.view(F, H, T, d) * 0.5
+    out.copy_(val.to(torch.bfloat16))
