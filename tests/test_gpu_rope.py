@@ -144,3 +144,60 @@ def test_rope_full_attention_then_decode():
             pos += t
     finally:
         st.close()
+
+
+def test_yarn_stack_layer_by_layer_and_whole_stack_calls():
+    """A three-layer stack with YaRN: frames 0-2 one call per layer (the real-model pattern),
+    frame 3 one call for all layers, then decoding one layer per call.  Every call rotates
+    its own layers' new keys; each layer is checked against the oracle on the GPU's state."""
+    from workloads import WorkloadConfig
+
+    wl = WorkloadConfig("yarn_stack", 3, 8, 2, 128, 24, 4, 40, "bf16", "iid", 5151, pos_offset=777)
+    spec = orc.rope_spec(wl.head_dim, 1e6, "yarn", factor=4.0, orig_max=4096, dtype="bf16")
+    st = FrameStepper.from_workload(wl, max_decode_tokens=4, rope="yarn", rope_theta=1e6, rope_factor=4.0,
+                                    rope_orig_max=4096)
+    T, L = wl.tokens_per_frame, wl.n_layers
+    try:
+        for n in range(wl.n_frames):
+            states = {l: gpu_state_as_oracle(st.read_state(l), "bf16") for l in range(L)}
+            q, k, v, host = frame_tensors(wl, n, list(range(L)))
+            out = torch.empty((L, wl.n_q_heads, T, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+            if n < 3:
+                for l in range(L):
+                    st.step(q[l:l + 1], k[l:l + 1], v[l:l + 1], out[l:l + 1], layer_begin=l, layer_count=1)
+            else:
+                st.step(q, k, v, out)
+            torch.cuda.synchronize()
+            for l in range(L):
+                x = host[l]
+                r = orc.frame_step(states[l], widen(x["q"], "bf16"), widen(x["k"], "bf16"), widen(x["v"], "bf16"), n,
+                                   wl.capacity, wl.scale, wl.pos_offset, rope=spec)
+                err = np.abs(out[l].float().cpu().numpy().astype(np.float64) - r.out)
+                assert err.max() <= TOL_O["bf16"][0] and err.mean() <= TOL_O["bf16"][1], \
+                    f"frame {n} layer {l}: output {err.max():.3e}"
+                ck, _, _ = st.read_cache(l)
+                assert _ulp_close(widen(ck[:, n * T:(n + 1) * T], "bf16"), r.k_stored, "bf16"), \
+                    f"frame {n} layer {l}: rotated keys in the cache"
+        say(f"  yarn stack: {wl.n_frames} frames ok")
+        rng = np.random.default_rng(5)
+        t = 2
+        pos = wl.pos_offset + wl.n_frames * T + np.arange(t)
+        for l in range(L):
+            qd = gen.f32_to_bf16_bits(rng.standard_normal((1, wl.n_q_heads, t, wl.head_dim)).astype(np.float32))
+            kd = gen.f32_to_bf16_bits(rng.standard_normal((1, wl.n_kv_heads, t, wl.head_dim)).astype(np.float32))
+            vd = gen.f32_to_bf16_bits(rng.standard_normal((1, wl.n_kv_heads, t, wl.head_dim)).astype(np.float32))
+            ck, cv, _ = st.read_cache(l)
+            o = torch.empty((1, wl.n_q_heads, t, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+            st.decode(to_device(qd, "bf16"), to_device(kd, "bf16"), to_device(vd, "bf16"), o, layer_begin=l,
+                      layer_count=1)
+            torch.cuda.synchronize()
+            hist_k = widen(ck[:, :wl.n_frames * T], "bf16")
+            hist_v = widen(cv[:, :wl.n_frames * T], "bf16")
+            want = orc.decode_attention(widen(qd[0], "bf16"), hist_k, hist_v, widen(kd[0], "bf16"),
+                                        widen(vd[0], "bf16"), wl.scale, rope=spec, positions=pos)
+            err = np.abs(o[0].float().cpu().numpy().astype(np.float64) - want)
+            assert err.max() <= TOL_O["bf16"][0] and err.mean() <= TOL_O["bf16"][1], f"decode layer {l}: {err.max():.3e}"
+            dk, _ = st.read_decode_rows(l)
+            assert _ulp_close(widen(dk[:, -t:], "bf16"), orc.rope_rotate(widen(kd[0], "bf16"), pos, spec), "bf16")
+    finally:
+        st.close()
