@@ -461,6 +461,7 @@ def main():
             "admitted_rows_per_head": round(admitted, 1),
             "GBps": round(refresh_gbs, 1),
             "peak_GBps": PEAK_HBM_GBS,
+            "frac": round(refresh_gbs / PEAK_HBM_GBS, 4),
         },
         "latency": {
             "frame_ms_median_state_full": round(med, 4),
