@@ -220,10 +220,12 @@ def decode_bench(wl, q_all, k_all, v_all, out, stream, n_calls=32):
             "frac": round(gbs / PEAK_HBM_GBS, 4), "append_ms_per_call": round(float(ms[:, 1].mean()), 4)}
 
 
-def large_bench(stream, name="vlm72b_80layer", timed=16):
+def large_bench(stream, name="vlm72b_80layer", timed=16, kv_heads=None):
     """The 72B-shaped stack (80 layers, 64 Q / 8 KV heads, 256 tokens/frame, capacity 4096,
     low-rank keys built on the device): the first frames fill the state, then `timed`
-    frames run at state full, all 80 layers per call.  Reported beside the 7B line."""
+    frames run at state full, all 80 layers per call.  Reported beside the 7B line.
+    kv_heads < 8 runs one GPU's share of a head-sharded stack (kv_heads KV heads and
+    their query heads on each GPU; the heads need nothing from each other)."""
     from paper_2605_31598_amd import FrameStepper
     from workloads import CONFIGS
     from workloads import device as wdev
@@ -231,6 +233,8 @@ def large_bench(stream, name="vlm72b_80layer", timed=16):
     import torch
 
     wl = CONFIGS[name]
+    if kv_heads is not None:
+        wl = wl.with_(n_kv_heads=kv_heads, n_q_heads=wl.group * kv_heads)
     L, Hq, Hkv, T, d = wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.tokens_per_frame, wl.head_dim
     fill = -(-wl.capacity // T)  # frames until the state is full
     F = fill + timed
@@ -264,7 +268,9 @@ def large_bench(stream, name="vlm72b_80layer", timed=16):
     alg = attention_flops(wl, wl.capacity)
     exe = executed_mfma_flops(wl, wl.capacity)
     frame_ms = stages.sum(axis=1)
-    res = {"workload": name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "tokens_per_frame": T,
+    shards = CONFIGS[name].n_kv_heads // wl.n_kv_heads
+    res = {"workload": name if shards == 1 else f"{name}, one GPU's share of {shards}-way KV-head sharding",
+           "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "tokens_per_frame": T,
            "capacity": wl.capacity, "inputs": "i.i.d. N(0,1) Q and V, low-rank keys (rank 16 + noise), bf16",
            "timed_frames_at_state_full": timed, "frames_per_s": round(timed / wall, 2),
            "ms_per_frame": round(1e3 * wall / timed, 4), "attention_ms": round(float(att.mean()), 4),
@@ -275,6 +281,25 @@ def large_bench(stream, name="vlm72b_80layer", timed=16):
            "flatness_max_dev": round(float(np.max(np.abs(frame_ms / np.median(frame_ms) - 1.0))), 4)}
     print(f"[bench] {name}: {res['frames_per_s']} frames/s at state full", file=sys.stderr, flush=True)
     return res
+
+
+def copy_bandwidth(n_bytes=1 << 30, reps=5):
+    """Read + write GB/s of the runtime's device-to-device copy of 1 GiB: the practical
+    streaming rate the refresh launch's GB/s is set against."""
+    import torch
+
+    src = torch.ones(n_bytes // 2, dtype=torch.int16, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    b.synchronize()
+    gbs = 2 * n_bytes * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    return round(gbs, 1)
 
 
 def cpu_baseline(wl, seconds):
@@ -475,6 +500,9 @@ def main():
         result["decode"] = decode_bench(wl, q_all, k_all, v_all, out, stream)
         result["diagnostics"] = diagnostics_bench(stream)
         result["vlm72b"] = large_bench(stream)
+        result["vlm72b_shard8"] = large_bench(stream, kv_heads=1)
+        result["hbm"]["copy_GBps"] = copy_bandwidth()
+        result["hbm"]["frac_of_copy"] = round(result["hbm"]["GBps"] / result["hbm"]["copy_GBps"], 4)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)
