@@ -175,7 +175,20 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
 
   // ---------------- staging (global -> registers -> LDS) ----------------
   u32x4 kpre[ITEMS], vpre[ITEMS];
-  auto load_tile = [&](int t, bool with_v) {
+  // pure: tile t lies wholly inside the state, so no key needs a test; thread
+  // tid's item it is row it * (kThreads / KCH) + tid / KCH, chunk tid % KCH.
+  const int base_off = (tid / KCH) * D + (tid % KCH) * 8;
+  auto load_tile = [&](int t, bool with_v, auto pure) {
+    if constexpr (decltype(pure)::value) {
+      const uint16_t* kt = kst + static_cast<size_t>(t) * kKT * D + base_off;
+      const uint16_t* vt = vst + static_cast<size_t>(t) * kKT * D + base_off;
+#pragma unroll
+      for (int it = 0; it < ITEMS; ++it) {
+        kpre[it] = *reinterpret_cast<const u32x4*>(kt + it * (kThreads / KCH) * D);
+        vpre[it] = with_v ? *reinterpret_cast<const u32x4*>(vt + it * (kThreads / KCH) * D) : u32x4{0u, 0u, 0u, 0u};
+      }
+      return;
+    }
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int idx = it * kThreads + tid;
@@ -223,9 +236,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
 
   // ============================ sweep 1: row statistics ============================
   float m = -1e30f, l = 0.f;
-  auto sweep1_tile = [&](int t, auto masked) {
+  auto sweep1_tile = [&](int t, auto masked, auto pure_next) {
     const int b = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1, false);
+    if (t + 1 < n_tiles) load_tile(t + 1, false, pure_next);
     if (active) {
 #pragma unroll
       for (int kb = 0; kb < kKT / 32; ++kb) {
@@ -256,11 +269,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (t + 1 < n_tiles) store_tile(b ^ 1, false);
     __syncthreads();
   };
-  load_tile(0, false);
+  load_tile(0, false, std::false_type{});
   store_tile(0, false);
   __syncthreads();
-  for (int t = 0; t < first_masked && t < n_tiles; ++t) sweep1_tile(t, std::false_type{});
-  for (int t = first_masked; t < n_tiles; ++t) sweep1_tile(t, std::true_type{});
+  for (int t = 0; t + 1 < first_masked; ++t) sweep1_tile(t, std::false_type{}, std::true_type{});
+  if (first_masked > 0) sweep1_tile(first_masked - 1, std::false_type{}, std::false_type{});
+  for (int t = first_masked; t < n_tiles; ++t) sweep1_tile(t, std::true_type{}, std::false_type{});
 
   // Row maximum (log2 units) and 1/sum.  Sweep 2 feeds the PV MFMA with
   // E = exp2(x - max) <= 1, whose largest entry is exactly 1 in bf16, and applies
@@ -286,9 +300,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const int tr_row = 4 * h + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  auto sweep2_tile = [&](int t, auto masked) {
+  auto sweep2_tile = [&](int t, auto masked, auto pure_next) {
     const int b = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1, true);
+    if (t + 1 < n_tiles) load_tile(t + 1, true, pure_next);
     if (active) {
 #pragma unroll
       for (int kb = 0; kb < kKT / 32; ++kb) {
@@ -346,11 +360,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
       }
     }
   };
-  load_tile(0, true);
+  load_tile(0, true, std::false_type{});
   store_tile(0, true);
   __syncthreads();
-  for (int t = 0; t < first_masked && t < n_tiles; ++t) sweep2_tile(t, std::false_type{});
-  for (int t = first_masked; t < n_tiles; ++t) sweep2_tile(t, std::true_type{});
+  for (int t = 0; t + 1 < first_masked; ++t) sweep2_tile(t, std::false_type{}, std::true_type{});
+  if (first_masked > 0) sweep2_tile(first_masked - 1, std::false_type{}, std::false_type{});
+  for (int t = first_masked; t < n_tiles; ++t) sweep2_tile(t, std::true_type{}, std::false_type{});
 
   // ---------------- output: O / sum, staged through LDS for 16-byte stores ----------------
   if (active && h == 0) sm.il[wave][l32] = inv_l;
