@@ -119,7 +119,20 @@ __global__ __launch_bounds__(kThreads, 1) void attn_full_kernel(AttnArgs a) {
 
   // ---------------- staging (global -> registers -> LDS) ----------------
   u32x4 kpre[ITEMS], vpre[ITEMS];
-  auto load_tile = [&](int t) {
+  // pure: tile t lies wholly among the cached keys, so no key needs a test; thread
+  // tid's item it is row it * (kThreads / KCH) + tid / KCH, chunk tid % KCH.
+  const int base_off = (tid / KCH) * D + (tid % KCH) * 8;
+  auto load_tile = [&](int t, auto pure) {
+    if constexpr (decltype(pure)::value) {
+      const uint16_t* kt = kst + static_cast<size_t>(t) * kKT * D + base_off;
+      const uint16_t* vt = vst + static_cast<size_t>(t) * kKT * D + base_off;
+#pragma unroll
+      for (int it = 0; it < ITEMS; ++it) {
+        kpre[it] = *reinterpret_cast<const u32x4*>(kt + it * (kThreads / KCH) * D);
+        vpre[it] = *reinterpret_cast<const u32x4*>(vt + it * (kThreads / KCH) * D);
+      }
+      return;
+    }
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int idx = it * kThreads + tid;
@@ -176,9 +189,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_full_kernel(AttnArgs a) {
   float m = -1e30f;  // running row maximum (logit units), the same in lanes l and l ^ 32
   float l = 0.f;     // this lane's share of the row sum of exp2((x - m) c)
 
-  auto sweep_tile = [&](int t, auto masked) {
+  auto sweep_tile = [&](int t, auto masked, auto pure_next) {
     const int b = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1);
+    if (t + 1 < n_tiles) load_tile(t + 1, pure_next);
     if (active) {
 #pragma unroll
       for (int kb = 0; kb < kKT / 32; ++kb) {
@@ -242,11 +255,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_full_kernel(AttnArgs a) {
     if (t + 1 < n_tiles) store_tile(b ^ 1);
     __syncthreads();
   };
-  load_tile(0);
+  load_tile(0, std::false_type{});
   store_tile(0);
   __syncthreads();
-  for (int t = 0; t < first_masked && t < n_tiles; ++t) sweep_tile(t, std::false_type{});
-  for (int t = first_masked; t < n_tiles; ++t) sweep_tile(t, std::true_type{});
+  for (int t = 0; t + 1 < first_masked; ++t) sweep_tile(t, std::false_type{}, std::true_type{});
+  if (first_masked > 0) sweep_tile(first_masked - 1, std::false_type{}, std::false_type{});
+  for (int t = first_masked; t < n_tiles; ++t) sweep_tile(t, std::true_type{}, std::false_type{});
 
   // ---------------- output: O^T / sum, staged through LDS for 16-byte stores ----------------
   const float lt = l + __shfl_xor(l, 32, 64);
