@@ -16,7 +16,9 @@
  *
  * Conventions shared by every entry point
  * ---------------------------------------
- * - Pointers named q, k, v, out are DEVICE pointers owned by the caller.
+ * - Pointers named q, k, v, out are DEVICE pointers owned by the caller, 16-byte
+ *   aligned (the kernels move 16-byte chunks); a misaligned one is
+ *   SKV_ERR_INVALID_ARG.
  * - Every device operation is enqueued on the HIP stream given to skv_init and
  *   is stream-ordered; no call blocks the host except skv_timing_stop.
  * - Errors are returned as skv_status; on error nothing is enqueued and the

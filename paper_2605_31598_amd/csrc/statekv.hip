@@ -37,6 +37,8 @@ skv_status fail(skv_status s, const std::string& msg) {
   return s;
 }
 
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 skv_status hip_fail(hipError_t e, const char* what) {
   g_last_error = std::string(what) + ": " + hipGetErrorString(e);
   return SKV_ERR_DEVICE;
@@ -353,6 +355,8 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
   if (q == nullptr || k == nullptr || v == nullptr || out == nullptr)
     return fail(SKV_ERR_INVALID_ARG, "q, k, v and out must be device pointers");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(SKV_ERR_INVALID_ARG, "q, k, v and out must be 16-byte aligned");
   const skv_config& c = ctx->cfg;
   if (layer_count < 1 || layer_begin < 0 || layer_begin + layer_count > c.n_layers)
     return fail(SKV_ERR_INVALID_ARG, "layer range outside [0, n_layers)");
@@ -463,6 +467,8 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
   if (q == nullptr || k == nullptr || v == nullptr || out == nullptr)
     return fail(SKV_ERR_INVALID_ARG, "q, k, v and out must be device pointers");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(SKV_ERR_INVALID_ARG, "q, k, v and out must be 16-byte aligned");
   const skv_config& c = ctx->cfg;
   if (layer_count < 1 || layer_begin < 0 || layer_begin + layer_count > c.n_layers)
     return fail(SKV_ERR_INVALID_ARG, "layer range outside [0, n_layers)");

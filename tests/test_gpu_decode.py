@@ -130,6 +130,8 @@ def test_decode_error_statuses():
                                    o.data_ptr()) == B.SKV_ERR_INVALID_ARG
         assert lib.skv_decode_step(st.ctx, 0, 1, 65, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                    o.data_ptr()) == B.SKV_ERR_INVALID_ARG
+        assert lib.skv_decode_step(st.ctx, 0, 1, 1, q.data_ptr(), k.data_ptr() + 8, v.data_ptr(),
+                                   o.data_ptr()) == B.SKV_ERR_INVALID_ARG  # misaligned key pointer
         q5, k5, v5, o5 = dec(5)
         with pytest.raises(StateKVError, match="CAPACITY"):
             st.decode(q5, k5, v5, o5)

@@ -153,6 +153,8 @@ def test_error_statuses_on_device():
             B.skv_frame_step(st.ctx, 0, 3, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr())
         with pytest.raises(StateKVError, match="SKV_ERR_INVALID_ARG"):
             B.skv_frame_step(st.ctx, 0, 2, q.data_ptr(), 0, v.data_ptr(), out.data_ptr())
+        with pytest.raises(StateKVError, match="SKV_ERR_INVALID_ARG"):  # misaligned by one bf16 element
+            B.skv_frame_step(st.ctx, 0, 2, q.data_ptr() + 2, k.data_ptr(), v.data_ptr(), out.data_ptr())
         st.step(q, k, v, out)
         st.step(q, k, v, out)
         with pytest.raises(StateKVError, match="SKV_ERR_CAPACITY"):
