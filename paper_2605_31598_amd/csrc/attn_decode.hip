@@ -32,7 +32,11 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int kDecWaves = 4;                  // independent waves per workgroup
 constexpr int kDecThreads = kDecWaves * 64;
-constexpr int kPadV = 16;                     // V row padding (bf16): transpose reads conflict-free
+// V row padding (bf16).  ds_read_b64_tr_b16 serves 32 lanes (four rows x 64 B) per
+// LDS pass over 64 four-byte banks; a row stride of 80 (D = 128) or 48 (D = 64)
+// dwords, modulo 64, puts those four rows on disjoint banks.  A 16-element pad
+// (72 dwords) overlaps them two-way.
+constexpr int kPadV = 32;
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }  // v_exp_f32
 

@@ -42,7 +42,11 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kRowsWave = kMfmaRowsPerWave;
 constexpr int kKT = 128;   // keys per LDS tile (four 32-key blocks)
 constexpr int kPadK = 8;   // K row padding (bf16): 16-byte reads conflict-free
-constexpr int kPadV = 16;  // V row padding (bf16): transpose reads conflict-free
+// V row padding (bf16).  ds_read_b64_tr_b16 serves 32 lanes (four rows x 64 B) per
+// LDS pass over 64 four-byte banks; a row stride of 80 (D = 128) or 48 (D = 64)
+// dwords, modulo 64, puts those four rows on disjoint banks.  A 16-element pad
+// (72 dwords) overlaps them two-way.
+constexpr int kPadV = 32;
 constexpr int kPadO = 8;   // output staging row padding (bf16)
 
 template <int D>
@@ -50,6 +54,7 @@ struct SmemFull {
   uint16_t k[2][kKT][D + kPadK];
   uint16_t v[2][kKT][D + kPadV];
 };
+static_assert(sizeof(SmemFull<128>) <= 160 * 1024, "gfx950 LDS per workgroup");
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }  // v_exp_f32
 

@@ -7,26 +7,33 @@
 // divides by T (the importance score of the attention-driven selection).
 //
 // Work decomposition
-//   * A workgroup owns 256 query rows of one (layer, KV head): 8 waves x 32 rows,
-//     two waves per SIMD.  Rows are the G query heads sharing the KV head times
-//     the T frame tokens (grouped-query packing: every row of the tile reads the
-//     same K/V).  Two waves per SIMD let the hardware run one wave's exp/softmax
-//     VALU work under the other wave's MFMAs; a single wave does not overlap its
-//     own MFMA and VALU streams well on gfx950.
+//   * A workgroup owns up to 256 query rows of one (layer, KV head): 8 waves x
+//     32 rows, two waves per SIMD.  Rows are the G query heads sharing the KV
+//     head times the T frame tokens (grouped-query packing: every row of the tile
+//     reads the same K/V).  Two waves per SIMD let the hardware run one wave's
+//     exp/softmax VALU work under the other wave's MFMAs.
+//   * A split workgroup (the short shares the host plan puts in the grid's last
+//     round) owns at most 128 rows; waves w and w + 4 take the same 32 rows and
+//     the first and the second half of every key tile, combine their row
+//     statistics after sweep 1 and their outputs at the end, so the last round
+//     also runs two waves per SIMD.
 //   * Keys stream through LDS in tiles of 128 (four 32-key blocks), double
-//     buffered, K and V both row-major; the next tile's global loads are issued
-//     before the current tile's compute.  A block's K (and V) operand reads are
-//     all issued before its MFMA chain, and waves raise their priority while
-//     issuing MFMAs so the other wave on the SIMD fills the VALU slots.
+//     buffered, K and V both row-major with padded rows.  The load unit copies
+//     the next tile global -> LDS (global_load_lds) while the current one is
+//     computed, with no registers or LDS store instructions.  Operand reads from
+//     LDS are issued ahead as inline assembly with explicit waits (V of a block
+//     during its exponentials, K of the next block during its PV MFMAs), and
+//     waves raise their priority while issuing MFMAs.
 //   * Two sweeps over the keys.  Sweep 1: S^T = K Q^T -> per-row max and sum of
 //     exp2.  Sweep 2: S^T again -> E = exp2(x - row max) -> O += E V (scaled by
 //     1/sum at the end) and per-key column sums of P = E / sum.  Exact
 //     probabilities are known only after the row statistics, and recomputing
 //     K Q^T is cheaper than storing the logits.
 //   * Tiles that contain frame keys (the only ones with masked entries) run in a
-//     separate loop, keeping mask code off the common path.
-//   * The blockIdx -> tile mapping keeps the row tiles of one (layer, KV head)
-//     on one XCD so they share K/V in that XCD's L2.
+//     separate loop, keeping mask code off the common path; tiles wholly inside
+//     the state are copied with per-lane offsets fixed once per launch.
+//   * The host plan keeps the row tiles of one (layer, KV head) on one XCD so
+//     they share K/V in that XCD's L2.
 //
 // MFMA v_mfma_f32_32x32x16_bf16 (wave64) operand layout, lane l, h = l / 32:
 //   A (32x16): A[l % 32][8h .. 8h+7]   B (16x32): B[8h .. 8h+7][l % 32]
@@ -41,6 +48,7 @@
 #include "internal.h"
 
 #include <type_traits>
+#include <utility>
 
 namespace skv {
 
@@ -57,7 +65,11 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kRowsWave = kMfmaRowsPerWave;
 constexpr int kKT = 128;       // keys per LDS tile (four 32-key blocks)
 constexpr int kPadK = 8;       // K row padding (bf16): 16-byte reads conflict-free
-constexpr int kPadV = 16;      // V row padding (bf16): transpose reads conflict-free
+// V row padding (bf16).  ds_read_b64_tr_b16 serves 32 lanes (four rows x 64 B) per
+// LDS pass over 64 four-byte banks; a row stride of 80 (D = 128) or 48 (D = 64)
+// dwords, modulo 64, puts those four rows on disjoint banks.  A 16-element pad
+// (72 dwords) overlaps them two-way.
+constexpr int kPadV = 32;
 constexpr int kPadO = 8;       // output staging row padding (bf16)
 
 template <int D>
@@ -67,6 +79,7 @@ struct Smem {
   float cs[2][kWaves][kKT];     // per-wave column sums of one tile
   float il[kWaves][kRowsWave];  // 1 / row sum, for the output
 };
+static_assert(sizeof(Smem<128>) <= 160 * 1024, "gfx950 LDS per workgroup");
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }  // v_exp_f32
 
@@ -74,6 +87,38 @@ template <int CTRL>
 __device__ inline float dpp_f(float x) {
   // DPP lane permutation inside rows of 16 lanes (all rows and banks enabled).
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+
+template <typename F, int... I>
+__device__ inline void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled with constant i
+template <int N, typename F>
+__device__ inline void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// ds_read_b64_tr_b16 at LDS byte address addr + OFF, issued as inline assembly:
+// the compiler then does not order it behind the outstanding global -> LDS copies
+// of the next tile (it cannot tell the two buffers apart).  The caller waits for
+// the result with lgkm_wait before use.
+template <int OFF>
+__device__ inline s16x4 ds_read_tr(uint32_t addr) {
+  s16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+template <int OFF>
+__device__ inline u32x4 ds_read_b128(uint32_t addr) {
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+// s_waitcnt lgkmcnt(N), ordered before every use of x
+template <int N, typename T>
+__device__ inline void lgkm_wait(T& x) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x) : "i"(N));
 }
 
 // Sum of cs[16] over the 32 lanes that share h = lane / 32 (the query rows of
@@ -121,8 +166,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = D / 16;                   // k-steps of K Q^T
   constexpr int DB = D / 32;                   // 32-column blocks of O
   constexpr int KCH = D / 8;                   // 16-byte chunks per K/V row
-  constexpr int ITEMS = kKT * KCH / kThreads;  // chunks of one tile staged per thread
-  static_assert(ITEMS * kThreads == kKT * KCH, "staging split");
 
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   Smem<D>& sm = *reinterpret_cast<Smem<D>*>(smem_raw);
@@ -141,7 +184,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const int n_tiles = (n_keys + kKT - 1) / kKT;
   const int first_masked = S / kKT;  // tiles from here on contain frame keys or the ragged end
   const int row_end = wk.row0 + wk.rows;  // rows of this workgroup: [wk.row0, row_end)
-  const int row0 = wk.row0 + wave * kRowsWave;
+  // split workgroup: waves w and w + 4 take the same 32 rows, the first and the
+  // second half of every key tile
+  const bool split = wk.split != 0;
+  const int grp = split ? (wave >> 2) : 0;
+  const int rb = split ? (wave & 3) : wave;  // 32-row block of the workgroup
+  const int key0 = grp * (kKT / 2);          // first key of this wave's share of a tile
+  const int row0 = wk.row0 + rb * kRowsWave;
   const bool active = row0 < row_end;
   const float c = a.scale_log2;
 
@@ -173,81 +222,125 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     }
   }
 
-  // ---------------- staging (global -> registers -> LDS) ----------------
-  u32x4 kpre[ITEMS], vpre[ITEMS];
-  // pure: tile t lies wholly inside the state, so no key needs a test; thread
-  // tid's item it is row it * (kThreads / KCH) + tid / KCH, chunk tid % KCH.
-  const int base_off = (tid / KCH) * D + (tid % KCH) * 8;
-  auto load_tile = [&](int t, bool with_v, auto pure) {
-    if constexpr (decltype(pure)::value) {
-      const uint16_t* kt = kst + static_cast<size_t>(t) * kKT * D + base_off;
-      const uint16_t* vt = vst + static_cast<size_t>(t) * kKT * D + base_off;
+  // ---------------- staging (global -> LDS by the load unit) ----------------
+  // global_load_lds_dwordx4: lane i of one instruction writes its 16 bytes at
+  // LDS base + 16 i, so one instruction fills 64 consecutive 16-byte slots of the
+  // padded tile.  A slot that falls on a row's padding re-loads chunk 0 of its
+  // row (padding is never read).  Keys past the end re-load the last key (finite
+  // input data; those keys are masked).
+  constexpr int KROW = (D + kPadK) / 8, VROW = (D + kPadV) / 8;  // 16-byte slots per padded row
+  constexpr int KINS = kKT * KROW / 64, VINS = kKT * VROW / 64;  // instructions per tile
+  static_assert(KINS * 64 == kKT * KROW && VINS * 64 == kKT * VROW, "whole instructions per tile");
+  constexpr int KIT = (KINS + kWaves - 1) / kWaves, VIT = (VINS + kWaves - 1) / kWaves;
+  int koff[KIT], voff[VIT];  // element offset of this lane's slot inside a tile (rows of D)
 #pragma unroll
-      for (int it = 0; it < ITEMS; ++it) {
-        kpre[it] = *reinterpret_cast<const u32x4*>(kt + it * (kThreads / KCH) * D);
-        vpre[it] = with_v ? *reinterpret_cast<const u32x4*>(vt + it * (kThreads / KCH) * D) : u32x4{0u, 0u, 0u, 0u};
+  for (int it = 0; it < KIT; ++it) {
+    const int q = (it * kWaves + wave) * 64 + lane;
+    const int ch = q % KROW;
+    koff[it] = (q / KROW) * D + (ch < KCH ? ch : 0) * 8;
+  }
+#pragma unroll
+  for (int it = 0; it < VIT; ++it) {
+    const int q = (it * kWaves + wave) * 64 + lane;
+    const int ch = q % VROW;
+    voff[it] = (q / VROW) * D + (ch < KCH ? ch : 0) * 8;
+  }
+  auto dma_one = [&](const uint16_t* src, uint16_t* dst_tile, int ins) {
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                     (void __attribute__((address_space(3)))*)(reinterpret_cast<char*>(dst_tile) + ins * 1024),
+                                     16, 0, 0);
+  };
+  // source of a key row (any key index; clamped to the last key)
+  auto key_src = [&](const uint16_t* st, const uint16_t* fr, int j) -> const uint16_t* {
+    j = j < n_keys ? j : n_keys - 1;
+    return j < S ? st + static_cast<size_t>(j) * D : fr + static_cast<size_t>(j - S) * D;
+  };
+  auto dma_tile = [&](int t, int b, bool with_v, auto pure) {
+#pragma unroll
+    for (int it = 0; it < KIT; ++it) {
+      const int ins = it * kWaves + wave;
+      if (ins < KINS) {
+        const uint16_t* src;
+        if constexpr (decltype(pure)::value) {
+          src = kst + static_cast<size_t>(t) * kKT * D + koff[it];
+        } else {
+          const int r = koff[it] / D;
+          src = key_src(kst, kfr, t * kKT + r) + (koff[it] - r * D);
+        }
+        dma_one(src, &sm.k[b][0][0], ins);
       }
-      return;
     }
+    if (!with_v) return;
 #pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const int idx = it * kThreads + tid;
-      const int kk = idx / KCH, ch = idx % KCH;
-      const int j = t * kKT + kk;
-      u32x4 x = {0u, 0u, 0u, 0u}, y = {0u, 0u, 0u, 0u};
-      if (j < S) {
-        x = *reinterpret_cast<const u32x4*>(kst + static_cast<size_t>(j) * D + ch * 8);
-        if (with_v) y = *reinterpret_cast<const u32x4*>(vst + static_cast<size_t>(j) * D + ch * 8);
-      } else if (j < n_keys) {
-        x = *reinterpret_cast<const u32x4*>(kfr + static_cast<size_t>(j - S) * D + ch * 8);
-        if (with_v) y = *reinterpret_cast<const u32x4*>(vfr + static_cast<size_t>(j - S) * D + ch * 8);
+    for (int it = 0; it < VIT; ++it) {
+      const int ins = it * kWaves + wave;
+      if (ins < VINS) {
+        const uint16_t* src;
+        if constexpr (decltype(pure)::value) {
+          src = vst + static_cast<size_t>(t) * kKT * D + voff[it];
+        } else {
+          const int r = voff[it] / D;
+          src = key_src(vst, vfr, t * kKT + r) + (voff[it] - r * D);
+        }
+        dma_one(src, &sm.v[b][0][0], ins);
       }
-      kpre[it] = x;
-      vpre[it] = y;
     }
   };
-  auto store_tile = [&](int b, bool with_v) {
-#pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const int idx = it * kThreads + tid;
-      const int kk = idx / KCH, ch = idx % KCH;
-      *reinterpret_cast<u32x4*>(&sm.k[b][kk][ch * 8]) = kpre[it];
-      if (with_v) *reinterpret_cast<u32x4*>(&sm.v[b][kk][ch * 8]) = vpre[it];
-    }
-  };
+  // the copies of a tile are in LDS once vmcnt drains; the barrier after this
+  // publishes them to the workgroup
+  auto dma_wait = [] { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
 
-  // S^T block (32 keys x 32 rows) for key block kb of buffer b.
-  auto qk = [&](int b, int kb) -> f32x16 {
+  // LDS operand reads are issued ahead as inline assembly with explicit waits:
+  // the V operand of block kb is read while block kb's exponentials run, the K
+  // operand of block kb + 1 during block kb's PV MFMAs and column sums (at most
+  // 15 reads are in flight, the reach of lgkmcnt).  A wait for one of these reads
+  // counts the reads issued after it; other LDS accesses in flight can only
+  // make such a wait longer.
+  auto lds_addr = [](const void* p) -> uint32_t {
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char*)p));
+  };
+  auto issue_k = [&](auto kbc, uint32_t kaddr, u32x4 (&kop)[KS]) {
+    constexpr int KB = decltype(kbc)::value;
+    static_for<KS>([&](auto ksc) {
+      constexpr int ks = decltype(ksc)::value;
+      kop[ks] = ds_read_b128<(KB * 32 * (D + kPadK) + ks * 16) * 2>(kaddr);
+    });
+  };
+  // S^T block from the K operand in kop; `later` = reads issued after kop's
+  auto qk_mfma = [&](u32x4 (&kop)[KS]) -> f32x16 {
     __builtin_amdgcn_s_setprio(1);
-    u32x4 kop[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kop[ks] = *reinterpret_cast<const u32x4*>(&sm.k[b][kb * 32 + l32][ks * 16 + h * 8]);
     f32x16 acc = {};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+    static_for<KS>([&](auto ksc) {
+      constexpr int ks = decltype(ksc)::value;
+      lgkm_wait<KS - 1 - ks>(kop[ks]);
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kop[ks]), qreg[ks], acc, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < KS; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
-#pragma unroll
-    for (int i = 0; i < KS; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    });
     __builtin_amdgcn_s_setprio(0);
     return acc;
   };
 
   // ============================ sweep 1: row statistics ============================
   float m = -1e30f, l = 0.f;
-  auto sweep1_tile = [&](int t, auto masked, auto pure_next) {
+  // NB = 32-key blocks of a tile this wave takes: 4, or 2 in a split workgroup
+  auto sweep1_tile = [&](int t, auto masked, auto pure_next, auto nbc) {
+    constexpr int NB = decltype(nbc)::value;
     const int b = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1, false, pure_next);
+    const uint32_t kaddr = lds_addr(&sm.k[b][key0 + l32][h * 8]);
+    u32x4 kop[KS];
+    if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
+    if (t + 1 < n_tiles) dma_tile(t + 1, b ^ 1, false, pure_next);
     if (active) {
-#pragma unroll
-      for (int kb = 0; kb < kKT / 32; ++kb) {
-        const f32x16 acc = qk(b, kb);
+      static_for<NB>([&](auto kbc) {
+        constexpr int KB = decltype(kbc)::value;
+        const f32x16 acc = qk_mfma(kop);
+        if constexpr (KB + 1 < NB) issue_k(std::integral_constant<int, KB + 1>{}, kaddr, kop);
+        f32x16 accv = acc;
+        asm volatile("" : "+v"(accv));  // keep the exponentials behind the reads just issued
         float z[16];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) z[v] = acc[v];
+        for (int v = 0; v < 16; ++v) z[v] = accv[v];
         if constexpr (decltype(masked)::value) {
-          const int rel = lim - (t * kKT + kb * 32 + 4 * h);
+          const int rel = lim - (t * kKT + key0 + KB * 32 + 4 * h);
 #pragma unroll
           for (int v = 0; v < 16; ++v)
             if (8 * (v >> 2) + (v & 3) > rel) z[v] = -__builtin_huge_valf();
@@ -264,17 +357,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
         // give exactly exp2(0) = 1.
         l = l * fast_exp2((m - mn) * c) + sum;
         m = mn;
-      }
+      });
     }
-    if (t + 1 < n_tiles) store_tile(b ^ 1, false);
+    if (t + 1 < n_tiles) dma_wait();
     __syncthreads();
   };
-  load_tile(0, false, std::false_type{});
-  store_tile(0, false);
+  auto sweep1 = [&](auto nbc) {
+    for (int t = 0; t + 1 < first_masked; ++t) sweep1_tile(t, std::false_type{}, std::true_type{}, nbc);
+    if (first_masked > 0) sweep1_tile(first_masked - 1, std::false_type{}, std::false_type{}, nbc);
+    for (int t = first_masked; t < n_tiles; ++t) sweep1_tile(t, std::true_type{}, std::false_type{}, nbc);
+  };
+
+  dma_tile(0, 0, false, std::false_type{});
+  dma_wait();
   __syncthreads();
-  for (int t = 0; t + 1 < first_masked; ++t) sweep1_tile(t, std::false_type{}, std::true_type{});
-  if (first_masked > 0) sweep1_tile(first_masked - 1, std::false_type{}, std::false_type{});
-  for (int t = first_masked; t < n_tiles; ++t) sweep1_tile(t, std::true_type{}, std::false_type{});
+  if (split)
+    sweep1(std::integral_constant<int, kKT / 64>{});
+  else
+    sweep1(std::integral_constant<int, kKT / 32>{});
 
   // Row maximum (log2 units) and 1/sum.  Sweep 2 feeds the PV MFMA with
   // E = exp2(x - max) <= 1, whose largest entry is exactly 1 in bf16, and applies
@@ -284,8 +384,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     // the other 16 keys of every 32-key block live in lane ^ 32
     const float mo = __shfl_xor(m, 32, 64);
     const float lo = __shfl_xor(l, 32, 64);
-    const float mm = fmaxf(m, mo);
-    const float ll = l * fast_exp2((m - mm) * c) + lo * fast_exp2((mo - mm) * c);
+    float mm = fmaxf(m, mo);
+    float ll = l * fast_exp2((m - mm) * c) + lo * fast_exp2((mo - mm) * c);
+    if (split) {
+      // the other key half of these rows is wave ^ 4's; exchanged through the
+      // second column-sum buffer, first written after sweep 2's first barrier
+      float* xm = &sm.cs[1][wave][0];
+      if (h == 0) {
+        xm[l32] = mm;
+        xm[32 + l32] = ll;
+      }
+      __syncthreads();
+      const float* pm = &sm.cs[1][wave ^ 4][0];
+      const float mp = pm[l32], lp = pm[32 + l32];
+      const float mt = fmaxf(mm, mp);
+      ll = ll * fast_exp2((mm - mt) * c) + lp * fast_exp2((mp - mt) * c);
+      mm = mt;
+    }
     mrow = row_valid ? mm * c : 0.f;
     inv_l = row_valid ? 1.0f / ll : 0.f;
   }
@@ -300,19 +415,37 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const int tr_row = 4 * h + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  auto sweep2_tile = [&](int t, auto masked, auto pure_next) {
+  auto sweep2_tile = [&](int t, auto masked, auto pure_next, auto nbc) {
+    constexpr int NB = decltype(nbc)::value;
     const int b = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1, true, pure_next);
+    const uint32_t kaddr = lds_addr(&sm.k[b][key0 + l32][h * 8]);
+    // LDS byte address of this lane's transpose-read position in buffer b
+    const uint32_t vaddr = lds_addr(&sm.v[b][key0 + tr_row][tr_col]);
+    u32x4 kop[KS];
+    if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
+    if (t + 1 < n_tiles) dma_tile(t + 1, b ^ 1, true, pure_next);
     if (active) {
-#pragma unroll
-      for (int kb = 0; kb < kKT / 32; ++kb) {
-        const f32x16 acc = qk(b, kb);
+      static_for<NB>([&](auto kbc) {
+        constexpr int KB = decltype(kbc)::value;
+        const int kb = key0 / 32 + KB;  // 32-key block of the tile
+        const f32x16 acc = qk_mfma(kop);
+        // V operand of this block, read while the exponentials run
+        bf16x8 vop[2][DB];
+        static_for<2 * DB>([&](auto ic) {
+          constexpr int s_ = decltype(ic)::value / DB, db = decltype(ic)::value % DB;
+          constexpr int r0 = KB * 32 + s_ * 16;
+          const s16x4 lo = ds_read_tr<(r0 * (D + kPadV) + db * 32) * 2>(vaddr);
+          const s16x4 hi = ds_read_tr<((r0 + 8) * (D + kPadV) + db * 32) * 2>(vaddr);
+          vop[s_][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        });
+        f32x16 accv = acc;
+        asm volatile("" : "+v"(accv));  // keep the exponentials behind the reads just issued
         const int rel = lim - (t * kKT + kb * 32 + 4 * h);
         bf16x8 pe[2];
         float cs[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float e = fast_exp2(fmaf(acc[v], c, -mrow));
+          float e = fast_exp2(fmaf(accv[v], c, -mrow));
           if constexpr (decltype(masked)::value) {
             if (8 * (v >> 2) + (v & 3) > rel) e = 0.f;
           }
@@ -320,58 +453,80 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
           cs[v] = e * inv_l;
         }
         __builtin_amdgcn_s_setprio(1);
-        bf16x8 vop[2][DB];
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const int r = kb * 32 + s * 16 + tr_row;
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(&sm.v[b][r][db * 32 + tr_col]));
-            const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(&sm.v[b][r + 8][db * 32 + tr_col]));
-            vop[s][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-          }
-        }
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int db = 0; db < DB; ++db) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pe[s], vop[s][db], o[db], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < 4 * DB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
-#pragma unroll
-        for (int i = 0; i < 2 * DB; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+        static_for<2 * DB>([&](auto ic) {
+          constexpr int i = decltype(ic)::value, s_ = i / DB, db = i % DB;
+          lgkm_wait<2 * (2 * DB - 1 - i)>(vop[s_][db]);
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pe[s_], vop[s_][db], o[db], 0, 0, 0);
+        });
+        // K operand of the next block, read during the PV MFMAs and the column sums
+        if constexpr (KB + 1 < NB) issue_k(std::integral_constant<int, KB + 1>{}, kaddr, kop);
         __builtin_amdgcn_s_setprio(0);
         const float tot = column_reduce(cs, lane);
         if ((lane & 1) == 0) sm.cs[b][wave][kb * 32 + key_lane] = tot;
-      }
+      });
     } else {
       for (int i = lane; i < kKT; i += 64) sm.cs[b][wave][i] = 0.f;
     }
-    if (t + 1 < n_tiles) store_tile(b ^ 1, true);
+    if (t + 1 < n_tiles) dma_wait();
     __syncthreads();
     // cross-wave column sums of tile t -> this row tile's partials; buffer b is
-    // written again only after the next barrier
+    // written again only after the next barrier.  In a split workgroup a key's
+    // sums come from the four waves of its half.
     if (tid < kKT) {
       const int j = t * kKT + tid;
       if (j < n_keys) {
         float sum = 0.f;
+        if (split) {
+          const int w0 = (tid / (kKT / 2)) * (kWaves / 2);
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) sum += sm.cs[b][w][tid];
+          for (int w = 0; w < kWaves / 2; ++w) sum += sm.cs[b][w0 + w][tid];
+        } else {
+#pragma unroll
+          for (int w = 0; w < kWaves; ++w) sum += sm.cs[b][w][tid];
+        }
         part[j] = sum;
       }
     }
   };
-  load_tile(0, true, std::false_type{});
-  store_tile(0, true);
+  auto sweep2 = [&](auto nbc) {
+    for (int t = 0; t + 1 < first_masked; ++t) sweep2_tile(t, std::false_type{}, std::true_type{}, nbc);
+    if (first_masked > 0) sweep2_tile(first_masked - 1, std::false_type{}, std::false_type{}, nbc);
+    for (int t = first_masked; t < n_tiles; ++t) sweep2_tile(t, std::true_type{}, std::false_type{}, nbc);
+  };
+  dma_tile(0, 0, true, std::false_type{});
+  dma_wait();
   __syncthreads();
-  for (int t = 0; t + 1 < first_masked; ++t) sweep2_tile(t, std::false_type{}, std::true_type{});
-  if (first_masked > 0) sweep2_tile(first_masked - 1, std::false_type{}, std::false_type{});
-  for (int t = first_masked; t < n_tiles; ++t) sweep2_tile(t, std::true_type{}, std::false_type{});
+  if (split)
+    sweep2(std::integral_constant<int, kKT / 64>{});
+  else
+    sweep2(std::integral_constant<int, kKT / 32>{});
+
+  // split workgroup: the second key half's waves hand their unnormalised output
+  // to the first half's (LDS holds no tile any more)
+  if (split) {
+    float* ox = reinterpret_cast<float*>(smem_raw);  // [row block][DB][16][64 lanes]
+    static_assert(kWaves / 2 * DB * 16 * 64 * 4 <= 2 * kKT * (D + kPadK) * 2, "exchange fits the K buffers");
+    if (grp == 1 && active) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) ox[((rb * DB + db) * 16 + v) * 64 + lane] = o[db][v];
+    }
+    __syncthreads();
+    if (grp == 0 && active) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[db][v] += ox[((rb * DB + db) * 16 + v) * 64 + lane];
+    }
+  }
+  const bool writer = active && grp == 0;
 
   // ---------------- output: O / sum, staged through LDS for 16-byte stores ----------------
-  if (active && h == 0) sm.il[wave][l32] = inv_l;
+  if (writer && h == 0) sm.il[wave][l32] = inv_l;
   __syncthreads();
   uint16_t* ost = reinterpret_cast<uint16_t*>(smem_raw) + static_cast<size_t>(wave) * kRowsWave * (D + kPadO);
-  if (active) {
+  if (writer) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int r = 8 * (v >> 2) + 4 * h + (v & 3);
@@ -382,7 +537,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     }
   }
   __syncthreads();
-  if (active) {
+  if (writer) {
     uint16_t* og = static_cast<uint16_t*>(a.out) + static_cast<size_t>(layer * a.H_q + g * a.G) * a.T * D;
 #pragma unroll
     for (int it = 0; it < kRowsWave * KCH / 64; ++it) {

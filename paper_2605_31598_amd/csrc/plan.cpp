@@ -12,7 +12,7 @@ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 // Appends ceil(blocks / max_chunk) workgroups of nearly equal block counts
 // covering blocks [first, first + blocks) of range lg.
 void split(std::vector<AttnWork>& out, std::vector<int32_t>& tiles, int lg, int first, int blocks, int max_chunk,
-           int rows, int rpw) {
+           int rows, int rpw, bool key_split) {
   if (blocks <= 0) return;
   const int n = ceil_div(blocks, max_chunk);
   int b = first;
@@ -20,14 +20,15 @@ void split(std::vector<AttnWork>& out, std::vector<int32_t>& tiles, int lg, int 
     const int nb = blocks / n + (i < blocks % n ? 1 : 0);
     const int row0 = b * rpw;
     const int row1 = std::min(rows, (b + nb) * rpw);
-    out.push_back({lg, row0, row1 - row0, tiles[lg]++});
+    out.push_back({lg, row0, row1 - row0, tiles[lg]++, key_split ? 1 : 0});
     b += nb;
   }
 }
 
 }  // namespace
 
-AttnPlan plan_attention(int n_lg, int rows, int rows_per_wave, int max_waves, int n_xcd, int cu_per_xcd) {
+AttnPlan plan_attention(int n_lg, int rows, int rows_per_wave, int max_waves, int n_xcd, int cu_per_xcd,
+                        bool split_short) {
   AttnPlan plan;
   plan.tiles.assign(static_cast<size_t>(std::max(n_lg, 0)), 0);
   if (n_lg <= 0 || rows <= 0) return plan;
@@ -45,7 +46,7 @@ AttnPlan plan_attention(int n_lg, int rows, int rows_per_wave, int max_waves, in
     std::vector<AttnWork>& out = lists[static_cast<size_t>(x)];
 
     if (static_cast<int64_t>(n) * ceil_div(nb, half) <= cu_per_xcd) {  // one round of short workgroups
-      for (int lg = lo; lg < hi; ++lg) split(out, plan.tiles, lg, 0, nb, half, rows, rows_per_wave);
+      for (int lg = lo; lg < hi; ++lg) split(out, plan.tiles, lg, 0, nb, half, rows, rows_per_wave, split_short);
       continue;
     }
     const int q = nb / max_waves, r = nb % max_waves;
@@ -70,15 +71,16 @@ AttnPlan plan_attention(int n_lg, int rows, int rows_per_wave, int max_waves, in
     }
     for (int i = 0; i < n; ++i)
       for (int w = 0; w < keep[static_cast<size_t>(i)]; ++w)
-        split(out, plan.tiles, lo + i, w * max_waves, max_waves, max_waves, rows, rows_per_wave);
+        split(out, plan.tiles, lo + i, w * max_waves, max_waves, max_waves, rows, rows_per_wave, false);
     for (int i = 0; i < n; ++i) {
       const int first = keep[static_cast<size_t>(i)] * max_waves;
-      split(out, plan.tiles, lo + i, first, nb - first, demote > 0 ? half : max_waves, rows, rows_per_wave);
+      split(out, plan.tiles, lo + i, first, nb - first, demote > 0 ? half : max_waves, rows, rows_per_wave,
+            demote > 0 && split_short);
     }
   }
   size_t longest = 0;
   for (const auto& l : lists) longest = std::max(longest, l.size());
-  plan.items.assign(longest * static_cast<size_t>(n_xcd), AttnWork{0, 0, 0, 0});
+  plan.items.assign(longest * static_cast<size_t>(n_xcd), AttnWork{0, 0, 0, 0, 0});
   for (size_t j = 0; j < longest; ++j)
     for (int x = 0; x < n_xcd; ++x)
       if (j < lists[static_cast<size_t>(x)].size())

@@ -13,9 +13,11 @@ namespace skv {
 
 // One workgroup's share: rows [row0, row0 + rows) of the packed G*T query rows
 // of (layer, KV head) `lg`; its column sums of P go to row-tile slot `tile`.
-// rows == 0 marks an empty slot (the workgroup exits at once).
+// rows == 0 marks an empty slot (the workgroup exits at once).  split != 0: at
+// most half a workgroup of row blocks, each covered by two waves that take one
+// half of every key tile each (two waves per SIMD on a short share of rows).
 struct AttnWork {
-  int32_t lg, row0, rows, tile;
+  int32_t lg, row0, rows, tile, split;
 };
 
 struct AttnPlan {
@@ -31,11 +33,14 @@ struct AttnPlan {
 // own L2.  Every (layer, KV head) stays on one XCD (its K/V rows are fetched
 // into that L2 once), and each XCD's list holds its full workgroups first and
 // its partial ones last.  When the full workgroups do not fill whole rounds of
-// the XCD's compute units, enough of them are broken into workgroups of at
-// most max_waves/2 waves (one wave per SIMD) that the last round holds only
-// such short workgroups.  If every range fits into one round of short
-// workgroups, all workgroups are short.
-AttnPlan plan_attention(int n_lg, int rows, int rows_per_wave, int max_waves, int n_xcd, int cu_per_xcd);
+// the XCD's compute units, enough of them are broken into short workgroups of
+// at most max_waves/2 row blocks that the last round holds only such short
+// workgroups.  If every range fits into one round of short workgroups, all
+// workgroups are short.  With split_short, short workgroups are marked split
+// (two waves per row block, one per key half); otherwise they run one wave per
+// row block.
+AttnPlan plan_attention(int n_lg, int rows, int rows_per_wave, int max_waves, int n_xcd, int cu_per_xcd,
+                        bool split_short);
 
 // Upper bound on plan.tiles[i] for any n_lg, n_xcd and cu_per_xcd.
 int plan_max_tiles(int rows, int rows_per_wave, int max_waves);

@@ -178,9 +178,11 @@ skv_status build_plans(skv_ctx* c, int rows) {
     const hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, c->device);
     if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
     const int n_xcd = (cu >= 8 && cu % 8 == 0) ? 8 : 1;  // workgroups go round-robin over the XCDs
+    // the full-attention kernel has no key-split mode
+    const bool split_short = cfg.policy != SKV_POLICY_FULL;
     for (int lc = 1; lc <= cfg.n_layers; ++lc)
       host[static_cast<size_t>(lc - 1)] = skv::plan_attention(lc * cfg.n_kv_heads, rows, skv::kMfmaRowsPerWave,
-                                                               skv::kMfmaWaves, n_xcd, cu / n_xcd);
+                                                               skv::kMfmaWaves, n_xcd, cu / n_xcd, split_short);
   } else {
     // fp32 path: every (layer, KV head) writes ceil(rows / 64) tiles; one
     // table of the largest call serves all calls

@@ -11,7 +11,9 @@ It is plain C++, so it is compiled here with g++ and run on the CPU:
 * all work of one (layer, KV head) lands on one XCD (workgroup i runs on XCD i % 8);
 * on each XCD the full workgroups come before the short ones;
 * for the 7B-shaped 28-layer stack on 256 compute units the full workgroups fill
-  exactly two rounds and the rest fits one round of <= 4-wave workgroups.
+  exactly two rounds and the rest fits one round of short workgroups (at most
+  four 32-row blocks), which are key-split when the caller allows it and never
+  otherwise.
 """
 import os
 import subprocess
@@ -27,10 +29,11 @@ DRIVER = r'''
 #include "plan.h"
 int main(int argc, char** argv) {
   const int n_lg = atoi(argv[1]), rows = atoi(argv[2]), n_xcd = atoi(argv[3]), cu = atoi(argv[4]);
-  const skv::AttnPlan p = skv::plan_attention(n_lg, rows, 32, 8, n_xcd, cu);
+  const bool split_short = atoi(argv[5]) != 0;
+  const skv::AttnPlan p = skv::plan_attention(n_lg, rows, 32, 8, n_xcd, cu, split_short);
   printf("bound %d\n", skv::plan_max_tiles(rows, 32, 8));
   for (size_t i = 0; i < p.tiles.size(); ++i) printf("tiles %zu %d\n", i, p.tiles[i]);
-  for (const auto& w : p.items) printf("item %d %d %d %d\n", w.lg, w.row0, w.rows, w.tile);
+  for (const auto& w : p.items) printf("item %d %d %d %d %d\n", w.lg, w.row0, w.rows, w.tile, w.split);
   return 0;
 }
 '''
@@ -45,9 +48,9 @@ def planner(tmp_path_factory):
     subprocess.run(["g++", "-O1", "-std=c++17", "-I", CSRC, str(src), os.path.join(CSRC, "plan.cpp"), "-o", str(exe)],
                    check=True)
 
-    def run(n_lg, rows, n_xcd=8, cu_per_xcd=32):
-        out = subprocess.run([str(exe), str(n_lg), str(rows), str(n_xcd), str(cu_per_xcd)], capture_output=True,
-                             text=True, check=True).stdout.split("\n")
+    def run(n_lg, rows, n_xcd=8, cu_per_xcd=32, split_short=True):
+        out = subprocess.run([str(exe), str(n_lg), str(rows), str(n_xcd), str(cu_per_xcd), str(int(split_short))],
+                             capture_output=True, text=True, check=True).stdout.split("\n")
         bound = int(out[0].split()[1])
         tiles = [int(l.split()[2]) for l in out if l.startswith("tiles")]
         items = [tuple(int(x) for x in l.split()[1:]) for l in out if l.startswith("item")]
@@ -62,17 +65,19 @@ SHAPES = [(112, 1372), (4, 1372), (640, 2048), (8, 2916), (2, 32), (28, 1372), (
 
 @pytest.mark.parametrize("n_lg,rows", SHAPES)
 @pytest.mark.parametrize("n_xcd,cu", [(8, 32), (1, 4), (8, 1)])
-def test_plan_covers_every_row_once(planner, n_lg, rows, n_xcd, cu):
-    bound, tiles, items = planner(n_lg, rows, n_xcd, cu)
+@pytest.mark.parametrize("split_short", [True, False])
+def test_plan_covers_every_row_once(planner, n_lg, rows, n_xcd, cu, split_short):
+    bound, tiles, items = planner(n_lg, rows, n_xcd, cu, split_short)
     assert len(tiles) == n_lg
     covered = [[] for _ in range(n_lg)]
     slots = [set() for _ in range(n_lg)]
     xcd_of = {}
-    for i, (lg, row0, nrows, tile) in enumerate(items):
+    for i, (lg, row0, nrows, tile, split) in enumerate(items):
         if nrows == 0:
             continue
         assert 0 <= lg < n_lg
         assert row0 % 32 == 0 and 0 < nrows <= 8 * 32 and row0 + nrows <= rows
+        assert split in (0, 1) and (split == 0 or (split_short and nrows <= 4 * 32))
         assert nrows % 32 == 0 or row0 + nrows == rows  # only the last wave of a range is ragged
         covered[lg].append((row0, row0 + nrows))
         assert tile not in slots[lg]
@@ -95,19 +100,22 @@ def test_full_workgroups_first_on_each_xcd(planner, n_lg, rows):
         assert full == sorted(full, reverse=True)
 
 
-def test_7b_stack_two_full_rounds_then_short_round(planner):
-    _, tiles, items = planner(28 * 4, 7 * 196)
+@pytest.mark.parametrize("split_short", [True, False])
+def test_7b_stack_two_full_rounds_then_short_round(planner, split_short):
+    _, tiles, items = planner(28 * 4, 7 * 196, split_short=split_short)
     real = [it for it in items if it[2] > 0]
     full = [it for it in real if it[2] == 256]
     short = [it for it in real if it[2] < 256]
     assert len(full) == 2 * 256
     assert len(short) <= 256 and all(it[2] <= 4 * 32 for it in short)
+    assert all(it[4] == 0 for it in full)
+    assert all(it[4] == int(split_short) for it in short)
     assert max(tiles) <= 7
 
 
 def test_small_call_uses_short_workgroups(planner):
-    # one layer of the 7B shape: 43 wave blocks per KV head fit one round of <= 4-wave workgroups
+    # one layer of the 7B shape: 43 wave blocks per KV head fit one round of short workgroups
     _, tiles, items = planner(4, 7 * 196)
     real = [it for it in items if it[2] > 0]
-    assert all(it[2] <= 128 for it in real)
+    assert all(it[2] <= 128 and it[4] == 1 for it in real)
     assert tiles == [11] * 4
