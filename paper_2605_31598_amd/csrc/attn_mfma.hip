@@ -21,9 +21,12 @@
 //     buffered, K and V both row-major with padded rows.  The load unit copies
 //     the next tile global -> LDS (global_load_lds) while the current one is
 //     computed, with no registers or LDS store instructions.  Operand reads from
-//     LDS are issued ahead as inline assembly with explicit waits (V of a block
-//     during its exponentials, K of the next block during its PV MFMAs), and
-//     waves raise their priority while issuing MFMAs.
+//     LDS are issued ahead as inline assembly with explicit waits, and waves
+//     raise their priority while issuing MFMAs.
+//   * Sweep 2 is software-pipelined over the blocks of a tile: block kb + 1's
+//     K Q^T MFMAs are issued interleaved with block kb's exponentials and block
+//     kb's PV MFMAs with its column sums (sched_group_barrier), so a wave's VALU
+//     work issues between its own dependent MFMAs instead of after them.
 //   * Two sweeps over the keys.  Sweep 1: S^T = K Q^T -> per-row max and sum of
 //     exp2.  Sweep 2: S^T again -> E = exp2(x - row max) -> O += E V (scaled by
 //     1/sum at the end) and per-key column sums of P = E / sum.  Exact
@@ -425,11 +428,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
     if (t + 1 < n_tiles) dma_tile(t + 1, b ^ 1, true, pure_next);
     if (active) {
+      // Software pipeline over the tile's blocks: block kb + 1's K Q^T MFMAs are
+      // issued interleaved with block kb's exponentials, block kb's PV MFMAs with
+      // its column sums, so the wave's VALU work issues between its own MFMAs.
+      f32x16 acc = qk_mfma(kop);
+      if constexpr (NB > 1) issue_k(std::integral_constant<int, 1>{}, kaddr, kop);
       static_for<NB>([&](auto kbc) {
         constexpr int KB = decltype(kbc)::value;
+        constexpr bool NEXT = KB + 1 < NB;
         const int kb = key0 / 32 + KB;  // 32-key block of the tile
-        const f32x16 acc = qk_mfma(kop);
-        // V operand of this block, read while the exponentials run
+        // wait for the next block's K operand (the latest reads), then read this block's V
+        if constexpr (NEXT) {
+          static_for<KS>([&](auto ksc) {
+            constexpr int ks = decltype(ksc)::value;
+            lgkm_wait<KS - 1 - ks>(kop[ks]);
+          });
+        }
         bf16x8 vop[2][DB];
         static_for<2 * DB>([&](auto ic) {
           constexpr int s_ = decltype(ic)::value / DB, db = decltype(ic)::value % DB;
@@ -438,31 +452,47 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
           const s16x4 hi = ds_read_tr<((r0 + 8) * (D + kPadV) + db * 32) * 2>(vaddr);
           vop[s_][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         });
-        f32x16 accv = acc;
-        asm volatile("" : "+v"(accv));  // keep the exponentials behind the reads just issued
+        f32x16 acc_next = {};
+        if constexpr (NEXT) {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            acc_next = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kop[ks]), qreg[ks],
+                                                               acc_next, 0, 0, 0);
+        }
         const int rel = lim - (t * kKT + kb * 32 + 4 * h);
         bf16x8 pe[2];
         float cs[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float e = fast_exp2(fmaf(accv[v], c, -mrow));
+          float e = fast_exp2(fmaf(acc[v], c, -mrow));
           if constexpr (decltype(masked)::value) {
             if (8 * (v >> 2) + (v & 3) > rel) e = 0.f;
           }
           pe[v >> 3][v & 7] = static_cast<__bf16>(e);
           cs[v] = e * inv_l;
         }
-        __builtin_amdgcn_s_setprio(1);
+        if constexpr (NEXT) {
+#pragma unroll
+          for (int i = 0; i < KS; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x402, 7, 0);
+          }
+        }
         static_for<2 * DB>([&](auto ic) {
           constexpr int i = decltype(ic)::value, s_ = i / DB, db = i % DB;
           lgkm_wait<2 * (2 * DB - 1 - i)>(vop[s_][db]);
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pe[s_], vop[s_][db], o[db], 0, 0, 0);
         });
-        // K operand of the next block, read during the PV MFMAs and the column sums
-        if constexpr (KB + 1 < NB) issue_k(std::integral_constant<int, KB + 1>{}, kaddr, kop);
-        __builtin_amdgcn_s_setprio(0);
+        // K operand two blocks ahead (this wave's kop registers are free again)
+        if constexpr (KB + 2 < NB) issue_k(std::integral_constant<int, KB + 2>{}, kaddr, kop);
         const float tot = column_reduce(cs, lane);
-        if ((lane & 1) == 0) sm.cs[b][wave][kb * 32 + key_lane] = tot;
+        sm.cs[b][wave][kb * 32 + key_lane] = tot;  // lanes l and l ^ 1 store the same total
+#pragma unroll
+        for (int i = 0; i < 2 * DB; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x402, 5, 0);
+        }
+        acc = acc_next;
       });
     } else {
       for (int i = lane; i < kKT; i += 64) sm.cs[b][wave][i] = 0.f;
