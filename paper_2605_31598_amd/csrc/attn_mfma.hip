@@ -186,6 +186,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const int S = a.S, n_keys = a.S + a.T;
   const int n_tiles = (n_keys + kKT - 1) / kKT;
   const int first_masked = S / kKT;  // tiles from here on contain frame keys or the ragged end
+  // key tiles of this work item: all, or its share [kt0, kt1) of a key-split plan
+  const int ks = wk.ks;
+  const int kt0 = static_cast<int>(static_cast<int64_t>(ks) * n_tiles / a.n_ks);
+  const int kt1 = static_cast<int>(static_cast<int64_t>(ks + 1) * n_tiles / a.n_ks);
   const int row_end = wk.row0 + wk.rows;  // rows of this workgroup: [wk.row0, row_end)
   // split workgroup: waves w and w + 4 take the same 32 rows, the first and the
   // second half of every key tile
@@ -331,7 +335,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     const uint32_t kaddr = lds_addr(&sm.k[b][key0 + l32][h * 8]);
     u32x4 kop[KS];
     if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
-    if (t + 1 < n_tiles) dma_tile(t + 1, b ^ 1, false, pure_next);
+    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, false, pure_next);
     if (active) {
       static_for<NB>([&](auto kbc) {
         constexpr int KB = decltype(kbc)::value;
@@ -362,28 +366,45 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
         m = mn;
       });
     }
-    if (t + 1 < n_tiles) dma_wait();
+    if (t + 1 < kt1) dma_wait();
     __syncthreads();
   };
   auto sweep1 = [&](auto nbc) {
-    for (int t = 0; t + 1 < first_masked; ++t) sweep1_tile(t, std::false_type{}, std::true_type{}, nbc);
-    if (first_masked > 0) sweep1_tile(first_masked - 1, std::false_type{}, std::false_type{}, nbc);
-    for (int t = first_masked; t < n_tiles; ++t) sweep1_tile(t, std::true_type{}, std::false_type{}, nbc);
+    const int tm = first_masked < kt1 ? first_masked : kt1;  // unmasked tiles end here
+    for (int t = kt0; t + 1 < tm; ++t) sweep1_tile(t, std::false_type{}, std::true_type{}, nbc);
+    if (kt0 < tm) sweep1_tile(tm - 1, std::false_type{}, std::false_type{}, nbc);
+    for (int t = kt0 > first_masked ? kt0 : first_masked; t < kt1; ++t)
+      sweep1_tile(t, std::true_type{}, std::false_type{}, nbc);
   };
-
-  dma_tile(0, 0, false, std::false_type{});
-  dma_wait();
-  __syncthreads();
-  if (split)
-    sweep1(std::integral_constant<int, kKT / 64>{});
-  else
-    sweep1(std::integral_constant<int, kKT / 32>{});
 
   // Row maximum (log2 units) and 1/sum.  Sweep 2 feeds the PV MFMA with
   // E = exp2(x - max) <= 1, whose largest entry is exactly 1 in bf16, and applies
   // 1/sum in fp32 to the output; the column sums use P = E / sum.
   float mrow, inv_l;
-  {
+  float* stats = a.stats + (static_cast<size_t>(lg) * a.n_ks) * (a.G * a.T) * 2;  // [ks][row] (max, sum)
+  if (a.mode == 2) {
+    // output launch of a key-split plan: merge the statistics of every key range
+    float mm = -1e30f, ll = 0.f;
+    if (row_valid) {
+      for (int s = 0; s < a.n_ks; ++s) {
+        const float* st = stats + (static_cast<size_t>(s) * (a.G * a.T) + r_lane) * 2;
+        const float ms = st[0], lsum = st[1];
+        const float mt = fmaxf(mm, ms);
+        ll = ll * fast_exp2((mm - mt) * c) + lsum * fast_exp2((ms - mt) * c);
+        mm = mt;
+      }
+    }
+    mrow = row_valid ? mm * c : 0.f;
+    inv_l = row_valid ? 1.0f / ll : 0.f;
+  } else {
+    if (kt0 < kt1) dma_tile(kt0, kt0 & 1, false, std::false_type{});
+    dma_wait();
+    __syncthreads();
+    if (split)
+      sweep1(std::integral_constant<int, kKT / 64>{});
+    else
+      sweep1(std::integral_constant<int, kKT / 32>{});
+
     // the other 16 keys of every 32-key block live in lane ^ 32
     const float mo = __shfl_xor(m, 32, 64);
     const float lo = __shfl_xor(l, 32, 64);
@@ -403,6 +424,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
       const float mt = fmaxf(mm, mp);
       ll = ll * fast_exp2((mm - mt) * c) + lp * fast_exp2((mp - mt) * c);
       mm = mt;
+    }
+    if (a.mode == 1) {
+      // statistics launch of a key-split plan: this key range's (max, sum) per row
+      if (h == 0 && grp == 0 && row_valid) {
+        float* st = stats + (static_cast<size_t>(ks) * (a.G * a.T) + r_lane) * 2;
+        st[0] = mm;
+        st[1] = ll;
+      }
+      return;
     }
     mrow = row_valid ? mm * c : 0.f;
     inv_l = row_valid ? 1.0f / ll : 0.f;
@@ -426,7 +456,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     const uint32_t vaddr = lds_addr(&sm.v[b][key0 + tr_row][tr_col]);
     u32x4 kop[KS];
     if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
-    if (t + 1 < n_tiles) dma_tile(t + 1, b ^ 1, true, pure_next);
+    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, true, pure_next);
     if (active) {
       // Software pipeline over the tile's blocks: block kb + 1's K Q^T MFMAs are
       // issued interleaved with block kb's exponentials, block kb's PV MFMAs with
@@ -497,7 +527,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     } else {
       for (int i = lane; i < kKT; i += 64) sm.cs[b][wave][i] = 0.f;
     }
-    if (t + 1 < n_tiles) dma_wait();
+    if (t + 1 < kt1) dma_wait();
     __syncthreads();
     // cross-wave column sums of tile t -> this row tile's partials; buffer b is
     // written again only after the next barrier.  In a split workgroup a key's
@@ -519,11 +549,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     }
   };
   auto sweep2 = [&](auto nbc) {
-    for (int t = 0; t + 1 < first_masked; ++t) sweep2_tile(t, std::false_type{}, std::true_type{}, nbc);
-    if (first_masked > 0) sweep2_tile(first_masked - 1, std::false_type{}, std::false_type{}, nbc);
-    for (int t = first_masked; t < n_tiles; ++t) sweep2_tile(t, std::true_type{}, std::false_type{}, nbc);
+    const int tm = first_masked < kt1 ? first_masked : kt1;
+    for (int t = kt0; t + 1 < tm; ++t) sweep2_tile(t, std::false_type{}, std::true_type{}, nbc);
+    if (kt0 < tm) sweep2_tile(tm - 1, std::false_type{}, std::false_type{}, nbc);
+    for (int t = kt0 > first_masked ? kt0 : first_masked; t < kt1; ++t)
+      sweep2_tile(t, std::true_type{}, std::false_type{}, nbc);
   };
-  dma_tile(0, 0, true, std::false_type{});
+  if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
   dma_wait();
   __syncthreads();
   if (split)
@@ -555,6 +587,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   // ---------------- output: O / sum, staged through LDS for 16-byte stores ----------------
   if (writer && h == 0) sm.il[wave][l32] = inv_l;
   __syncthreads();
+  if (a.mode == 2) {
+    // this key range's share of O (already divided by the merged sum), fp32
+    if (writer) {
+      float* op = a.opart + static_cast<size_t>(ks) * a.n_layers * a.H_q * a.T * D +
+                  static_cast<size_t>(layer * a.H_q + g * a.G) * a.T * D;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = 8 * (v >> 2) + 4 * h + (v & 3);
+        const float sc = sm.il[wave][r];
+        if (row0 + r < row_end) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) op[static_cast<size_t>(row0 + r) * D + db * 32 + l32] = o[db][v] * sc;
+        }
+      }
+    }
+    return;
+  }
   uint16_t* ost = reinterpret_cast<uint16_t*>(smem_raw) + static_cast<size_t>(wave) * kRowsWave * (D + kPadO);
   if (writer) {
 #pragma unroll

@@ -30,6 +30,14 @@ struct AttnArgs {
   const float* rope_tab;  // null: no rotation; else rotate Q by {cos, sin} per (relative position,
                           // pair); kf holds the frame's keys already rotated
   int rope_pos0;          // relative position of frame token 0 (n * T)
+  // Key-split plans (MFMA kernel): the launch with mode 1 writes each work
+  // item's (row max, sum of exp2) over its key range to `stats`, the launch with
+  // mode 2 merges them, writes the column sums of its key range and its fp32
+  // share of O to `opart`; workgroups of the refresh launch then add the shares.
+  int mode;               // 0: whole key range in one launch; 1: statistics; 2: output share
+  int n_ks;               // key splits of the plan (1: none)
+  float* stats;           // [n_layers * H_kv][n_ks][G * T][2]
+  float* opart;           // [n_ks][n_layers][H_q][T][d]
 };
 
 // The refresh launch finishes a frame for `n_layers` layers: score finalisation,
@@ -57,6 +65,13 @@ struct RefreshArgs {
   int32_t frame_pos0;        // virtual position of frame token 0
   float inv_T;
   int mode;                  // 0: Top-B by score, 1: the B most recent, 2: append only
+  // key-split attention plans: n_comb more workgroups write the attention
+  // output, the sum of the n_ks fp32 shares (AttnArgs::opart), as bf16
+  int n_ks;                  // 1: no key split, no combine workgroups
+  int n_comb;
+  const float* opart;        // [n_ks][out_elems]
+  void* out;                 // [out_elems] bf16
+  int64_t out_elems;         // a multiple of 4
 };
 
 // Decode over the detailed cache (split-key flash decoding).  Each wave of the
@@ -88,6 +103,7 @@ constexpr int kDecodeMaxTokens = 64;  // new tokens per decode call
 constexpr int kDecodeItems = 2048;    // split items aimed at per call: one wave per SIMD slot of the
                                       // 256-CU device at two waves per SIMD (partials sized for it)
 
+constexpr int kMaxKeySplits = 16;       // key ranges of a key-split attention plan, at most
 constexpr int kMfmaRowsPerWave = 32;    // query rows (G*T packed) per attention wave
 constexpr int kMfmaWaves = 8;           // waves per attention workgroup (at most)
 constexpr int kSimpleRowsPerTile = 64;

@@ -18,11 +18,13 @@ namespace skv {
 // half of every key tile each (two waves per SIMD on a short share of rows).
 struct AttnWork {
   int32_t lg, row0, rows, tile, split;
+  int32_t ks;  // key split: the workgroup covers key tiles [ks * n / n_ks, (ks + 1) * n / n_ks)
 };
 
 struct AttnPlan {
   std::vector<AttnWork> items;  // one per workgroup, in launch order
   std::vector<int32_t> tiles;   // row tiles written for each (layer, KV head)
+  int32_t n_ks = 1;             // key splits (> 1: statistics, output and combine launches)
 };
 
 // Splits n_lg ranges of `rows` query rows into workgroups of at most
@@ -39,8 +41,13 @@ struct AttnPlan {
 // workgroups are short.  With split_short, short workgroups are marked split
 // (two waves per row block, one per key half); otherwise they run one wave per
 // row block.
+//
+// Calls too small to fill the device (full row workgroups for at most a third
+// of its compute units, up to max_key_splits > 1) split the keys instead: each
+// full row workgroup is repeated for n_ks key ranges, and the (layer-head, key
+// range) groups go round-robin over the XCDs.
 AttnPlan plan_attention(int n_lg, int rows, int rows_per_wave, int max_waves, int n_xcd, int cu_per_xcd,
-                        bool split_short);
+                        bool split_short, int max_key_splits);
 
 // Upper bound on plan.tiles[i] for any n_lg, n_xcd and cu_per_xcd.
 int plan_max_tiles(int rows, int rows_per_wave, int max_waves);

@@ -330,23 +330,47 @@ __device__ void append_frame(const RefreshArgs& a, int lg) {
   }
 }
 
+// Output of a key-split attention plan: out = the sum, in split order, of the
+// splits' fp32 shares, rounded once to bf16; workgroup c of n_comb takes every
+// n_comb-th group of four values.
+__device__ void combine_output(const RefreshArgs& a, int c) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  const int64_t n4 = a.out_elems / 4;
+  const int64_t stride = static_cast<int64_t>(a.n_comb) * blockDim.x;
+  for (int64_t i = static_cast<int64_t>(c) * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    f32x4 acc = reinterpret_cast<const f32x4*>(a.opart)[i];
+    for (int k = 1; k < a.n_ks; ++k) acc += reinterpret_cast<const f32x4*>(a.opart + static_cast<size_t>(k) * n4 * 4)[i];
+    unsigned short b[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = __builtin_bit_cast(unsigned short, static_cast<__bf16>(acc[j]));
+    const uint2 w = {static_cast<unsigned>(b[0]) | (static_cast<unsigned>(b[1]) << 16),
+                     static_cast<unsigned>(b[2]) | (static_cast<unsigned>(b[3]) << 16)};
+    reinterpret_cast<uint2*>(a.out)[i] = w;
+  }
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kSelectThreads) void refresh_kernel(RefreshArgs a) {
   extern __shared__ uint32_t pool_mem[];  // [pool] score bits, then [pool] positions
   __shared__ SelectShared sh;
   const int n_sel = a.mode == 2 ? 0 : a.n_layers * a.H_kv;
-  if (static_cast<int>(blockIdx.x) < n_sel) {
-    refresh_state(a, blockIdx.x, sh, pool_mem);
+  const int n_app = a.n_layers * a.H_kv;
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < n_sel) {
+    refresh_state(a, b, sh, pool_mem);
+  } else if (b < n_sel + n_app) {
+    append_frame(a, b - n_sel);
   } else {
-    append_frame(a, blockIdx.x - n_sel);
+    combine_output(a, b - n_sel - n_app);
   }
 }
 
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s) {
   const bool select = a.mode != 2;
   const size_t lds = select ? static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t) : 0;
-  hipLaunchKernelGGL(refresh_kernel, dim3((select ? 2 : 1) * a.n_layers * a.H_kv), dim3(kSelectThreads), lds, s, a);
+  const int grid = (select ? 2 : 1) * a.n_layers * a.H_kv + (a.n_ks > 1 ? a.n_comb : 0);
+  hipLaunchKernelGGL(refresh_kernel, dim3(grid), dim3(kSelectThreads), lds, s, a);
   return hipGetLastError();
 }
 

@@ -83,8 +83,11 @@ struct skv_ctx {
     const skv::AttnWork* work = nullptr;
     const int32_t* tiles = nullptr;  // row tiles per (layer, KV head) of the call
     int n_work = 0;
+    int n_ks = 1;                    // key splits (calls too small to fill the device)
   };
   std::vector<Plan> plans;
+  float* split_stats = nullptr;    // key-split plans: per-range row statistics and output shares,
+  float* split_out = nullptr;      // sized for the largest such plan (null if none)
   std::vector<void*> allocations;
 
   // progress of the stream
@@ -178,11 +181,13 @@ skv_status build_plans(skv_ctx* c, int rows) {
     const hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, c->device);
     if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
     const int n_xcd = (cu >= 8 && cu % 8 == 0) ? 8 : 1;  // workgroups go round-robin over the XCDs
-    // the full-attention kernel has no key-split mode
+    // the full-attention kernel has no split workgroups and no key splits
     const bool split_short = cfg.policy != SKV_POLICY_FULL;
+    const int max_ks = split_short ? skv::kMaxKeySplits : 1;
     for (int lc = 1; lc <= cfg.n_layers; ++lc)
       host[static_cast<size_t>(lc - 1)] = skv::plan_attention(lc * cfg.n_kv_heads, rows, skv::kMfmaRowsPerWave,
-                                                               skv::kMfmaWaves, n_xcd, cu / n_xcd, split_short);
+                                                               skv::kMfmaWaves, n_xcd, cu / n_xcd, split_short,
+                                                               max_ks);
   } else {
     // fp32 path: every (layer, KV head) writes ceil(rows / 64) tiles; one
     // table of the largest call serves all calls
@@ -202,6 +207,7 @@ skv_status build_plans(skv_ctx* c, int rows) {
     skv_ctx::Plan& d = c->plans[i];
     d.work = reinterpret_cast<const skv::AttnWork*>(static_cast<char*>(dev) + off);
     d.n_work = static_cast<int>(p.items.size());
+    d.n_ks = p.n_ks;
     if (!p.items.empty()) std::memcpy(blob.data() + off, p.items.data(), p.items.size() * sizeof(skv::AttnWork));
     off += p.items.size() * sizeof(skv::AttnWork);
     d.tiles = reinterpret_cast<const int32_t*>(static_cast<char*>(dev) + off);
@@ -213,6 +219,20 @@ skv_status build_plans(skv_ctx* c, int rows) {
   if (bytes > 0) {
     const hipError_t e = hipMemcpy(dev, blob.data(), bytes, hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy of the attention plans");
+  }
+  // buffers of the key-split plans
+  size_t stats_floats = 0, out_floats = 0;
+  for (size_t i = 0; i < host.size(); ++i) {
+    const size_t lc = i + 1, n_ks = static_cast<size_t>(host[i].n_ks);
+    if (n_ks < 2) continue;
+    stats_floats = std::max(stats_floats, lc * cfg.n_kv_heads * n_ks * static_cast<size_t>(rows) * 2);
+    out_floats = std::max(out_floats, n_ks * lc * cfg.n_q_heads * cfg.tokens_per_frame * cfg.head_dim);
+  }
+  if (stats_floats > 0) {
+    s = alloc(c, stats_floats * sizeof(float), reinterpret_cast<void**>(&c->split_stats));
+    if (s != SKV_OK) return s;
+    s = alloc(c, out_floats * sizeof(float), reinterpret_cast<void**>(&c->split_out));
+    if (s != SKV_OK) return s;
   }
   return SKV_OK;
 }
@@ -411,6 +431,10 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.tile_stride = ctx->tile_stride;
   aa.pool_stride = ctx->pool_stride;
   aa.scale_log2 = ctx->scale_log2;
+  aa.mode = 0;
+  aa.n_ks = plan.n_ks;
+  aa.stats = ctx->split_stats;
+  aa.opart = ctx->split_out;
 
   skv::RefreshArgs ra;
   ra.partial = aa.partial;
@@ -440,15 +464,31 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.frame_pos0 = pos0;
   ra.inv_T = 1.0f / static_cast<float>(T);
   ra.mode = c.policy == SKV_POLICY_STATEKV ? 0 : (c.policy == SKV_POLICY_RECENT ? 1 : 2);
+  // key-split plans: the refresh launch also adds the attention's output shares
+  ra.n_ks = ctx->use_mfma && !full ? plan.n_ks : 1;
+  ra.opart = ctx->split_out;
+  ra.out = out;
+  ra.out_elems = static_cast<int64_t>(layer_count) * c.n_q_heads * T * d;
+  ra.n_comb = static_cast<int>(std::min<int64_t>(128, (ra.out_elems / 4 + skv::kSelectThreads - 1) / skv::kSelectThreads));
 
   hipError_t e = mark(0);
   if (e == hipSuccess && ctx->rope_tab != nullptr)
     e = skv::launch_rope_keys(k, ctx->rope_keys, layer_count * Hkv, T, static_cast<int>(rb), ctx->elem, ctx->rope_tab,
                               static_cast<int>(ctx->frame * T), ctx->stream);
-  if (e == hipSuccess)
-    e = !ctx->use_mfma ? skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream)
-        : full         ? skv::launch_attention_full_bf16(aa, d, ctx->stream)
-                       : skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+  if (e == hipSuccess) {
+    if (!ctx->use_mfma) {
+      e = skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream);
+    } else if (full) {
+      e = skv::launch_attention_full_bf16(aa, d, ctx->stream);
+    } else if (plan.n_ks > 1) {  // key-split plan: statistics, output shares, their sum
+      aa.mode = 1;
+      e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+      aa.mode = 2;
+      if (e == hipSuccess) e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+    } else {
+      e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+    }
+  }
   if (e == hipSuccess) e = mark(1);
   if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
   if (e == hipSuccess) e = mark(2);

@@ -129,8 +129,9 @@ def oracle_step(wl, state, raw, frame):
                           frame, wl.capacity, wl.scale, wl.pos_offset)
 
 
-def run_tracking(wl, n_frames, layers, start_frame=0, forced=None, independent=True, log_every=1):
-    """Stream frames through the GPU (all layers per call).  Every frame and every
+def run_tracking(wl, n_frames, layers, start_frame=0, forced=None, independent=True, log_every=1, per_layer=False):
+    """Stream frames through the GPU (all layers per call, or one call per layer
+    with `per_layer`, the real-model calling pattern).  Every frame and every
     checked layer is compared with the oracle run on the GPU's own state entering
     that frame (so a near-tie cannot derail later frames).  With `independent`, the
     oracle also evolves its own state, and the first frame where the two states
@@ -155,7 +156,11 @@ def run_tracking(wl, n_frames, layers, start_frame=0, forced=None, independent=T
             before = {l: gpu_state_as_oracle(stepper.read_state(l), wl.dtype) for l in layers}
             if n % log_every == 0:
                 say(f"  [{wl.name}] frame {n} (state {before[layers[0]].size}) layers {list(layers)}")
-            stepper.step(q, k, v, out)
+            if per_layer:
+                for l in range(L):
+                    stepper.step(q[l:l + 1], k[l:l + 1], v[l:l + 1], out[l:l + 1], layer_begin=l, layer_count=1)
+            else:
+                stepper.step(q, k, v, out)
             out_h = out.float().cpu().numpy().astype(np.float64)
             for l in layers:
                 res = oracle_step(wl, before[l], host[l], n)

@@ -104,6 +104,19 @@ def test_full_size_one_frame_on_forced_full_state(name, layers, frame):
     say(f"{name} frame {frame}: {s}")
 
 
+PER_LAYER = [("vlm7b_28layer", [0, 27], 40), ("vlm72b_80layer", [0, 79], 20)]
+
+
+@pytest.mark.parametrize("name,layers,frame", PER_LAYER, ids=[f[0] for f in PER_LAYER])
+def test_full_size_one_layer_per_call_on_forced_full_state(name, layers, frame):
+    """Real-model calling pattern at full size: one call per layer, each too small to
+    fill the device, so the attention splits the keys over 10 (7B) or 4 (72B) ranges."""
+    wl = CONFIGS[name]
+    forced = {l: recent_state(wl, l, frame) for l in layers}
+    s = run_tracking(wl, 2, layers, start_frame=frame, forced=forced, independent=False, per_layer=True)
+    say(f"{name} frames {frame}-{frame + 1}, one layer per call: {s}")
+
+
 def test_vlm7b_28layer_stream_through_state_full():
     """First 14 frames of the 28-layer stack (state full from frame 11), layers 0 and 27 checked."""
     wl = CONFIGS["vlm7b_28layer"]

@@ -30,10 +30,12 @@ DRIVER = r'''
 int main(int argc, char** argv) {
   const int n_lg = atoi(argv[1]), rows = atoi(argv[2]), n_xcd = atoi(argv[3]), cu = atoi(argv[4]);
   const bool split_short = atoi(argv[5]) != 0;
-  const skv::AttnPlan p = skv::plan_attention(n_lg, rows, 32, 8, n_xcd, cu, split_short);
+  const int max_ks = atoi(argv[6]);
+  const skv::AttnPlan p = skv::plan_attention(n_lg, rows, 32, 8, n_xcd, cu, split_short, max_ks);
   printf("bound %d\n", skv::plan_max_tiles(rows, 32, 8));
+  printf("n_ks %d\n", p.n_ks);
   for (size_t i = 0; i < p.tiles.size(); ++i) printf("tiles %zu %d\n", i, p.tiles[i]);
-  for (const auto& w : p.items) printf("item %d %d %d %d %d\n", w.lg, w.row0, w.rows, w.tile, w.split);
+  for (const auto& w : p.items) printf("item %d %d %d %d %d %d\n", w.lg, w.row0, w.rows, w.tile, w.split, w.ks);
   return 0;
 }
 '''
@@ -48,13 +50,17 @@ def planner(tmp_path_factory):
     subprocess.run(["g++", "-O1", "-std=c++17", "-I", CSRC, str(src), os.path.join(CSRC, "plan.cpp"), "-o", str(exe)],
                    check=True)
 
-    def run(n_lg, rows, n_xcd=8, cu_per_xcd=32, split_short=True):
-        out = subprocess.run([str(exe), str(n_lg), str(rows), str(n_xcd), str(cu_per_xcd), str(int(split_short))],
-                             capture_output=True, text=True, check=True).stdout.split("\n")
+    def run(n_lg, rows, n_xcd=8, cu_per_xcd=32, split_short=True, max_ks=1, with_ks=False):
+        out = subprocess.run([str(exe), str(n_lg), str(rows), str(n_xcd), str(cu_per_xcd), str(int(split_short)),
+                              str(max_ks)], capture_output=True, text=True, check=True).stdout.split("\n")
         bound = int(out[0].split()[1])
+        n_ks = int(out[1].split()[1])
         tiles = [int(l.split()[2]) for l in out if l.startswith("tiles")]
         items = [tuple(int(x) for x in l.split()[1:]) for l in out if l.startswith("item")]
-        return bound, tiles, items
+        if with_ks:
+            return bound, n_ks, tiles, items
+        assert n_ks == 1 and all(it[5] == 0 for it in items)
+        return bound, tiles, [it[:5] for it in items]
 
     return run
 
@@ -119,3 +125,45 @@ def test_small_call_uses_short_workgroups(planner):
     real = [it for it in items if it[2] > 0]
     assert all(it[2] <= 128 and it[4] == 1 for it in real)
     assert tiles == [11] * 4
+
+
+# ---- key-split plans (calls too small to fill the device) ----
+
+@pytest.mark.parametrize("n_lg,rows", [(4, 1372), (8, 1372), (12, 1372), (8, 2048), (1, 37), (3, 1), (2, 32 * 8 * 3)])
+@pytest.mark.parametrize("n_xcd,cu", [(8, 32), (1, 4), (2, 8)])
+@pytest.mark.parametrize("split_short", [True, False])
+def test_key_split_plan_covers_rows_once_per_key_range(planner, n_lg, rows, n_xcd, cu, split_short):
+    bound, n_ks, tiles, items = planner(n_lg, rows, n_xcd, cu, split_short, 16, with_ks=True)
+    row_wgs = n_lg * -(-(-(-rows // 32)) // 8)  # full workgroups
+    if 3 * row_wgs > n_xcd * cu:
+        assert n_ks == 1
+        return
+    assert n_ks == min(16, n_xcd * cu // row_wgs) and n_ks >= 3
+    covered = {}
+    xcd_of = {}
+    for i, (lg, row0, nrows, tile, split, ks) in enumerate(items):
+        if nrows == 0:
+            continue
+        assert split == 0 and 0 <= ks < n_ks and 0 < nrows <= 256 and row0 % 32 == 0
+        covered.setdefault((lg, ks), []).append((row0, row0 + nrows, tile))
+        assert xcd_of.setdefault((lg, ks), i % n_xcd) == i % n_xcd, "one key range split over XCDs"
+    assert set(covered) == {(lg, ks) for lg in range(n_lg) for ks in range(n_ks)}
+    for (lg, ks), spans in covered.items():
+        spans.sort()
+        assert spans[0][0] == 0 and spans[-1][1] == rows
+        assert all(a[1] == b[0] for a, b in zip(spans, spans[1:]))
+        # the row tile slot of a row range is the same for every key range
+        assert [sp[2] for sp in spans] == list(range(len(spans))) == list(range(tiles[lg]))
+        assert tiles[lg] <= bound
+
+
+def test_key_splits_for_one_layer_of_the_7b_stack(planner):
+    # 4 (layer, KV head) ranges of 43 wave blocks: 24 row workgroups, 10 key ranges, all 8 XCDs busy
+    _, n_ks, tiles, items = planner(4, 7 * 196, 8, 32, True, 16, with_ks=True)
+    assert n_ks == 10 and tiles == [6] * 4
+    real = [it for it in items if it[2] > 0]
+    assert len(real) == 240 and all(it[4] == 0 for it in real)
+    assert {i % 8 for i, it in enumerate(items) if it[2] > 0} == set(range(8))
+    # the whole 28-layer stack fills the device without splitting keys
+    _, n_ks, _, _ = planner(28 * 4, 7 * 196, 8, 32, True, 16, with_ks=True)
+    assert n_ks == 1
