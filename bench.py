@@ -220,6 +220,42 @@ def decode_bench(wl, q_all, k_all, v_all, out, stream, n_calls=32):
             "frac": round(gbs / PEAK_HBM_GBS, 4), "append_ms_per_call": round(float(ms[:, 1].mean()), 4)}
 
 
+def per_layer_bench(wl, q_all, k_all, v_all, out, stream, n_frames=16):
+    """The real-model calling pattern: one skv_frame_step per layer (a model interleaves its
+    projections and MLP between them), timed at state full.  A one-layer call is too small to
+    fill the device, so its attention splits the keys (statistics, output shares, and their sum
+    in the refresh launch)."""
+    from paper_2605_31598_amd import FrameStepper
+    import torch
+
+    L, first = wl.n_layers, wl.full_from_frame + 4
+    st = FrameStepper.from_workload(wl, stream=stream)
+
+    def frames(f0):
+        for f in range(f0, f0 + n_frames):
+            for l in range(L):
+                st.step(q_all[f][l:l + 1], k_all[f][l:l + 1], v_all[f][l:l + 1], out[l:l + 1],
+                        layer_begin=l, layer_count=1)
+
+    try:
+        for f in range(first):
+            st.step(q_all[f], k_all[f], v_all[f], out)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        frames(first)  # wall clock, no events
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        st.timing_start(n_frames * L)  # then the same number of frames with per-call events
+        frames(first + n_frames)
+        ms = st.timing_stop(n_frames * L).astype(np.float64)
+    finally:
+        st.close()
+    return {"layers_per_call": 1, "timed_frames_at_state_full": n_frames, "frames_per_s": round(n_frames / wall, 2),
+            "ms_per_frame": round(1e3 * wall / n_frames, 4),
+            "attention_ms_per_call": round(float(ms[:, 0].mean()), 4),
+            "refresh_ms_per_call": round(float(ms[:, 1].mean()), 4)}
+
+
 def large_bench(stream, name="vlm72b_80layer", timed=16, kv_heads=None):
     """The 72B-shaped stack (80 layers, 64 Q / 8 KV heads, 256 tokens/frame, capacity 4096,
     low-rank keys built on the device): the first frames fill the state, then `timed`
@@ -498,6 +534,7 @@ def main():
     if not args.no_baselines:
         result["baselines"] = baselines(wl, q_all, k_all, v_all, out, stream, med)
         result["decode"] = decode_bench(wl, q_all, k_all, v_all, out, stream)
+        result["per_layer"] = per_layer_bench(wl, q_all, k_all, v_all, out, stream)
         result["diagnostics"] = diagnostics_bench(stream)
         result["vlm72b"] = large_bench(stream)
         result["vlm72b_shard8"] = large_bench(stream, kv_heads=1)
