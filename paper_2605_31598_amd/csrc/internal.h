@@ -42,13 +42,18 @@ struct AttnArgs {
 
 // The refresh launch finishes a frame for `n_layers` layers: score finalisation,
 // Top-B selection and state update in one workgroup per (layer, KV head), the
-// decode-cache append in a second set of workgroups of the same grid.
+// decode-cache append in a second set of workgroups of the same grid (either
+// set can be left out), and the sum of a key-split attention's output shares
+// in a third.
 struct RefreshArgs {
   const float* partial;      // as in AttnArgs
   const int32_t* lg_tiles;   // [n_layers][H_kv] row tiles the attention launch wrote
   int tile_stride, pool_stride;
-  const void* kf;            // [n_layers][H_kv][T][d]   frame keys
-  const void* vf;            //                          frame values
+  const void* kf;            // [n_layers][H_kv][kf_rows][d]   frame keys: the caller's input
+  const void* vf;            //   (kf_rows = T) or the frame's rows of the decode cache (max_tokens)
+  int64_t kf_rows;           // row stride of one (layer, KV head) block of kf / vf
+  bool select;               // workgroups for the selection and the state update
+  bool append;               // workgroups for the decode-cache append
   void* ks;                  // [n_layers][H_kv][B][d]   state slots
   void* vs;
   int32_t* state_pos;        // [n_layers][H_kv][B]
@@ -64,7 +69,7 @@ struct RefreshArgs {
   int row_bytes;             // d * element size, a multiple of 16
   int32_t frame_pos0;        // virtual position of frame token 0
   float inv_T;
-  int mode;                  // 0: Top-B by score, 1: the B most recent, 2: append only
+  int mode;                  // selection rule: 0: Top-B by score, 1: the B most recent
   // key-split attention plans: n_comb more workgroups write the attention
   // output, the sum of the n_ks fp32 shares (AttnArgs::opart), as bf16
   int n_ks;                  // 1: no key split, no combine workgroups

@@ -1,6 +1,6 @@
-// Frame refresh (Eq. 4 and Eq. 6): one launch, two kinds of workgroup.
+// Frame refresh (Eq. 4 and Eq. 6): one launch, up to three kinds of workgroup.
 //
-// Workgroups 0 .. L*H_kv-1, one per (layer, KV head), refresh the compressed state
+// Selection workgroups, one per (layer, KV head), refresh the compressed state
 // (mode 0: attention-driven selection; mode 1, the recency-window baseline: the
 // same steps with the position as the selection key):
 // 1. Finalise the importance scores of the candidate pool (state slots, then the
@@ -16,9 +16,11 @@
 // 4. Pair evicted state slots (then free slots S, S+1, ...) with admitted frame
 //    tokens in ascending order using block-wide scans, then copy the admitted
 //    K/V rows into those slots.  Retained slots never move.
-// Workgroups L*H_kv .. 2*L*H_kv-1 append the frame's K/V rows of one (layer, KV
-// head) to the decode cache D (the detailed state), concurrently with the above.
-// Mode 2 (streaming full attention, no compressed state) launches only these.
+// Append workgroups, one per (layer, KV head), copy the frame's K/V rows to the
+// decode cache D (the detailed state), concurrently with the above.  Streaming
+// full attention (no compressed state) launches only these; a launch that
+// selects after an earlier append reads the frame's rows back from D.
+// Combine workgroups add the output shares of a key-split attention plan.
 #include "internal.h"
 
 namespace skv {
@@ -278,7 +280,7 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
 
   // State update: admitted frame rows into their slots, 16-byte chunks.
   const int chunks = a.row_bytes >> 4;
-  const size_t src_base = static_cast<size_t>(lg) * T * a.row_bytes;
+  const size_t src_base = static_cast<size_t>(lg) * a.kf_rows * a.row_bytes;
   const size_t dst_base = static_cast<size_t>(lg) * B * a.row_bytes;
   for (int idx = tid; idx < count * chunks; idx += blockDim.x) {
     const int i = idx / chunks;
@@ -302,7 +304,7 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
 __device__ void append_frame(const RefreshArgs& a, int lg) {
   const int rb = a.row_bytes;
   const int n16 = a.T * (rb >> 4);  // 16-byte chunks of the block
-  const size_t src = static_cast<size_t>(lg) * a.T * rb;
+  const size_t src = static_cast<size_t>(lg) * a.kf_rows * rb;
   const size_t dst = (static_cast<size_t>(lg) * a.max_tokens + a.first_row) * rb;
   const char* kf = static_cast<const char*>(a.kf) + src;
   const char* vf = static_cast<const char*>(a.vf) + src;
@@ -354,8 +356,8 @@ __device__ void combine_output(const RefreshArgs& a, int c) {
 __global__ __launch_bounds__(kSelectThreads) void refresh_kernel(RefreshArgs a) {
   extern __shared__ uint32_t pool_mem[];  // [pool] score bits, then [pool] positions
   __shared__ SelectShared sh;
-  const int n_sel = a.mode == 2 ? 0 : a.n_layers * a.H_kv;
-  const int n_app = a.n_layers * a.H_kv;
+  const int n_sel = a.select ? a.n_layers * a.H_kv : 0;
+  const int n_app = a.append ? a.n_layers * a.H_kv : 0;
   const int b = static_cast<int>(blockIdx.x);
   if (b < n_sel) {
     refresh_state(a, b, sh, pool_mem);
@@ -367,9 +369,9 @@ __global__ __launch_bounds__(kSelectThreads) void refresh_kernel(RefreshArgs a) 
 }
 
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s) {
-  const bool select = a.mode != 2;
-  const size_t lds = select ? static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t) : 0;
-  const int grid = (select ? 2 : 1) * a.n_layers * a.H_kv + (a.n_ks > 1 ? a.n_comb : 0);
+  const size_t lds = a.select ? static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t) : 0;
+  const int grid = ((a.select ? 1 : 0) + (a.append ? 1 : 0)) * a.n_layers * a.H_kv + (a.n_ks > 1 ? a.n_comb : 0);
+  if (grid == 0) return hipSuccess;
   hipLaunchKernelGGL(refresh_kernel, dim3(grid), dim3(kSelectThreads), lds, s, a);
   return hipGetLastError();
 }

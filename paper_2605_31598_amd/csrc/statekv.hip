@@ -443,6 +443,9 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.pool_stride = ctx->pool_stride;
   ra.kf = k_used;
   ra.vf = v;
+  ra.kf_rows = T;
+  ra.select = !full;
+  ra.append = true;
   ra.ks = static_cast<char*>(ctx->state_k) + lh0 * B * rb;
   ra.vs = static_cast<char*>(ctx->state_v) + lh0 * B * rb;
   ra.state_pos = ctx->state_pos + lh0 * B;
@@ -463,7 +466,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.row_bytes = static_cast<int>(rb);
   ra.frame_pos0 = pos0;
   ra.inv_T = 1.0f / static_cast<float>(T);
-  ra.mode = c.policy == SKV_POLICY_STATEKV ? 0 : (c.policy == SKV_POLICY_RECENT ? 1 : 2);
+  ra.mode = c.policy == SKV_POLICY_RECENT ? 1 : 0;
   // key-split plans: the refresh launch also adds the attention's output shares
   ra.n_ks = ctx->use_mfma && !full ? plan.n_ks : 1;
   ra.opart = ctx->split_out;
@@ -576,7 +579,9 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   ra.H_kv = Hkv;
   ra.T = t;
   ra.row_bytes = static_cast<int>(rb);
-  ra.mode = 2;
+  ra.kf_rows = t;
+  ra.select = false;  // append only
+  ra.append = true;
 
   const bool timing = ctx->timing_n < ctx->timing_max;
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
