@@ -386,11 +386,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     // output launch of a key-split plan: merge the statistics of every key range
     float mm = -1e30f, ll = 0.f;
     if (row_valid) {
-      for (int s = 0; s < a.n_ks; ++s) {
-        const float* st = stats + (static_cast<size_t>(s) * (a.G * a.T) + r_lane) * 2;
-        const float ms = st[0], lsum = st[1];
-        const float mt = fmaxf(mm, ms);
-        ll = ll * fast_exp2((mm - mt) * c) + lsum * fast_exp2((ms - mt) * c);
+      // all loads first, then the merge in split order
+      float ms[kMaxKeySplits], lsum[kMaxKeySplits];
+#pragma unroll
+      for (int s = 0; s < kMaxKeySplits; ++s) {
+        ms[s] = -1e30f;
+        lsum[s] = 0.f;
+        if (s < a.n_ks) {
+          const float* st = stats + (static_cast<size_t>(s) * (a.G * a.T) + r_lane) * 2;
+          ms[s] = st[0];
+          lsum[s] = st[1];
+        }
+      }
+#pragma unroll
+      for (int s = 0; s < kMaxKeySplits; ++s) {
+        const float mt = fmaxf(mm, ms[s]);
+        ll = ll * fast_exp2((mm - mt) * c) + lsum[s] * fast_exp2((ms[s] - mt) * c);
         mm = mt;
       }
     }

@@ -192,8 +192,13 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
   constexpr int kJ = 4, kTB = 8;
   for (int j0 = tid; j0 < P; j0 += kJ * static_cast<int>(blockDim.x)) {
     float acc[kJ];
+    int32_t pos[kJ];  // loaded with the first batch of tiles
 #pragma unroll
-    for (int q = 0; q < kJ; ++q) acc[q] = 0.f;
+    for (int q = 0; q < kJ; ++q) {
+      acc[q] = 0.f;
+      const int j = j0 + q * static_cast<int>(blockDim.x);
+      pos[q] = j < S ? state_pos[j] : a.frame_pos0 + (j - S);
+    }
     for (int t0 = 0; t0 < n_tiles; t0 += kTB) {
       float v[kJ][kTB];
 #pragma unroll
@@ -214,11 +219,10 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
       const int j = j0 + q * static_cast<int>(blockDim.x);
       if (j < P) {
         const float s = acc[q] * a.inv_T;
-        const int32_t pos = j < S ? state_pos[j] : a.frame_pos0 + (j - S);
         pscore[j] = s;
-        ppos[j] = pos;
+        ppos[j] = pos[q];
         sbits[j] = __float_as_uint(s);
-        spos[j] = pos;
+        spos[j] = pos[q];
       }
     }
   }
