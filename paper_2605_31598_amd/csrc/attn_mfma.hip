@@ -124,19 +124,23 @@ __device__ inline void lgkm_wait(T& x) {
   asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x) : "i"(N));
 }
 
-// Sum of cs[16] over the 32 lanes that share h = lane / 32 (the query rows of
-// one half-block).  Returns, in every lane, the total of the key
+// Weighted sum of e[16] over the 32 lanes that share h = lane / 32 (the query
+// rows of one half-block), each lane's values scaled by its row's weight.
+// Returns, in every lane, the total of the key
 //   key(lane) = 8 * (b3 + 2 * b4) + 4 * h + (b1 + 2 * b2)     (bN = bit N of lane)
 // within the 32-key block; lanes differing only in bit 0 return the same key.
 // Reduce-scatter: each step halves the values a lane carries while pairing
-// lanes that differ in one more row bit.
-__device__ inline float column_reduce(const float (&cs)[16], int lane) {
+// lanes that differ in one more row bit.  The first step pairs lanes l and
+// l ^ 16 and applies the weights: w0 and w1 are the weights of the first and the
+// second value the swap leaves in this lane (own and partner row for b4 = 0,
+// partner and own row for b4 = 1).
+__device__ inline float column_reduce(const float (&e)[16], int lane, float w0, float w1) {
   float c1[8];
 #pragma unroll
   for (int v = 0; v < 8; ++v) {  // rows 0<->1 and 2<->3: lanes l and l^16
-    const auto pr = __builtin_amdgcn_permlane16_swap(__float_as_uint(cs[v]), __float_as_uint(cs[v + 8]),
+    const auto pr = __builtin_amdgcn_permlane16_swap(__float_as_uint(e[v]), __float_as_uint(e[v + 8]),
                                                      false, false);
-    c1[v] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+    c1[v] = fmaf(__uint_as_float(pr[0]), w0, __uint_as_float(pr[1]) * w1);
   }
   const bool b3 = lane & 8, b2 = lane & 4, b1 = lane & 2;
   float c2[4];
@@ -455,6 +459,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   for (int db = 0; db < DB; ++db) o[db] = f32x16{};
 
   const int key_lane = 8 * (((lane >> 3) & 1) + 2 * ((lane >> 4) & 1)) + 4 * h + (((lane >> 1) & 1) + 2 * ((lane >> 2) & 1));
+  // column-sum weights (1 / row sum) of the two rows the first reduction step meets
+  const float il_partner = __shfl_xor(inv_l, 16, 64);
+  const float w0 = (lane & 16) ? il_partner : inv_l, w1 = (lane & 16) ? inv_l : il_partner;
   // transpose-read coordinates of this lane inside its 16-lane group
   const int tr_row = 4 * h + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -510,7 +517,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
             if (8 * (v >> 2) + (v & 3) > rel) e = 0.f;
           }
           pe[v >> 3][v & 7] = static_cast<__bf16>(e);
-          cs[v] = e * inv_l;
+          cs[v] = e;
         }
         if constexpr (NEXT) {
 #pragma unroll
@@ -526,7 +533,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
         });
         // K operand two blocks ahead (this wave's kop registers are free again)
         if constexpr (KB + 2 < NB) issue_k(std::integral_constant<int, KB + 2>{}, kaddr, kop);
-        const float tot = column_reduce(cs, lane);
+        const float tot = column_reduce(cs, lane, w0, w1);
         sm.cs[b][wave][kb * 32 + key_lane] = tot;  // lanes l and l ^ 1 store the same total
 #pragma unroll
         for (int i = 0; i < 2 * DB; ++i) {
