@@ -47,14 +47,18 @@ __device__ inline int block_exclusive_count(bool flag, int* wave_count, int* tot
   return before + within;
 }
 
+constexpr int kLdsAdmit = 1024;  // frames up to this many tokens keep the admit lists in LDS
+
 struct SelectShared {
-  uint32_t hist[256];
+  uint32_t hist[2][256];  // radix passes alternate between the two
   uint32_t wave_min[kSelectThreads / 64];
   uint32_t wave_max[kSelectThreads / 64];
-  int wave_count[kSelectThreads / 64];
-  uint32_t lo, hi, count;
-  int remaining;
-  int digit;
+  int wave_active[kSelectThreads / 64];
+  int wave_count[kSelectThreads / 64];  // block_exclusive_count
+  int digit[2], remaining[2];           // one slot per pass parity
+  uint32_t count[2];
+  int32_t admit_src[kLdsAdmit];  // frame token of the a-th admitted candidate
+  int32_t admit_dst[kLdsAdmit];  // state slot it goes to
 };
 
 struct RadixResult {
@@ -79,10 +83,15 @@ __device__ inline int wave_sum_i32(int x) {
 // Radix select over the active entries j < n: the rank-th largest key
 // (1 <= rank <= number of active entries).  Digits of 8 bits start below the
 // leading bits that all active keys share.
+//
+// Two barriers per pass: pass p counts into hist[p % 2] (cleared two passes
+// earlier, or at entry) and publishes its digit in slot p % 2, which pass p + 2
+// overwrites only after every thread has passed pass p + 1's first barrier.
 template <typename KeyFn, typename ActiveFn>
 __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active, SelectShared& sh) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_waves = blockDim.x >> 6;
+  for (int i = tid; i < 2 * 256; i += blockDim.x) sh.hist[i >> 8][i & 255] = 0u;
   uint32_t lo = 0xFFFFFFFFu, hi = 0u;
   int cnt = 0;
   for (int j = tid; j < n; j += blockDim.x) {
@@ -99,47 +108,43 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
   if (lane == 0) {
     sh.wave_min[wave] = lo;
     sh.wave_max[wave] = hi;
-    sh.wave_count[wave] = cnt;
+    sh.wave_active[wave] = cnt;
   }
   __syncthreads();
-  if (tid == 0) {
-    uint32_t l = 0xFFFFFFFFu, h = 0u, c = 0u;
-    for (int w = 0; w < n_waves; ++w) {
-      l = min(l, sh.wave_min[w]);
-      h = max(h, sh.wave_max[w]);
-      c += static_cast<uint32_t>(sh.wave_count[w]);
-    }
-    sh.lo = l;
-    sh.hi = h;
-    sh.count = c;
+  // every thread combines the per-wave values itself
+  uint32_t l = 0xFFFFFFFFu, h = 0u;
+  int n_active = 0;
+  for (int w = 0; w < n_waves; ++w) {
+    l = min(l, sh.wave_min[w]);
+    h = max(h, sh.wave_max[w]);
+    n_active += sh.wave_active[w];
   }
-  __syncthreads();
-  const uint32_t any_key = sh.hi;
-  const uint32_t diff = sh.lo ^ sh.hi;
-  const int n_active = static_cast<int>(sh.count);
-  __syncthreads();
-  if (diff == 0u) return {any_key, rank, n_active};  // all active keys are equal
+  const uint32_t diff = l ^ h;
+  if (diff == 0u) {  // all active keys are equal
+    __syncthreads();  // the per-wave values are read before a next call writes them
+    return {h, rank, n_active};
+  }
 
   const int top_bit = 31 - __clz(static_cast<int>(diff));  // highest bit where active keys differ
-  uint32_t prefix = top_bit == 31 ? 0u : (any_key >> (top_bit + 1)) << (top_bit + 1);
+  uint32_t prefix = top_bit == 31 ? 0u : (h >> (top_bit + 1)) << (top_bit + 1);
   int remaining = rank;
   int equal = n_active;
-  for (int shift = top_bit + 1; shift > 0;) {
+  int par = 0;
+  for (int shift = top_bit + 1; shift > 0; par ^= 1) {
     const int width = shift >= 8 ? 8 : shift;
     shift -= width;
     const uint32_t dmask = (1u << width) - 1u;
     const uint32_t fixed = ~((dmask << shift) | ((1u << shift) - 1u));  // bits already decided
-    for (int i = tid; i < 256; i += blockDim.x) sh.hist[i] = 0u;
-    __syncthreads();
+    uint32_t* hist = sh.hist[par];
     for (int j = tid; j < n; j += blockDim.x) {
       if (!active(j)) continue;
       const uint32_t k = key(j);
-      if ((k & fixed) == prefix) atomicAdd(&sh.hist[(k >> shift) & dmask], 1u);
+      if ((k & fixed) == prefix) atomicAdd(&hist[(k >> shift) & dmask], 1u);
     }
     __syncthreads();
     if (tid < 64) {
       uint32_t c[4];
-      for (int b = 0; b < 4; ++b) c[b] = sh.hist[4 * tid + b];
+      for (int b = 0; b < 4; ++b) c[b] = hist[4 * tid + b];
       const uint32_t mine = c[0] + c[1] + c[2] + c[3];
       uint32_t suffix = mine;  // sum over lanes >= tid
       for (int off = 1; off < 64; off <<= 1) {
@@ -149,18 +154,18 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
       uint32_t above = suffix - mine;  // keys in higher bins
       for (int b = 3; b >= 0; --b) {
         if (above < static_cast<uint32_t>(remaining) && static_cast<uint32_t>(remaining) <= above + c[b]) {
-          sh.digit = 4 * tid + b;
-          sh.remaining = remaining - static_cast<int>(above);
-          sh.count = c[b];
+          sh.digit[par] = 4 * tid + b;
+          sh.remaining[par] = remaining - static_cast<int>(above);
+          sh.count[par] = c[b];
         }
         above += c[b];
       }
     }
     __syncthreads();
-    prefix |= static_cast<uint32_t>(sh.digit) << shift;
-    remaining = sh.remaining;
-    equal = static_cast<int>(sh.count);
-    __syncthreads();
+    prefix |= static_cast<uint32_t>(sh.digit[par]) << shift;
+    remaining = sh.remaining[par];
+    equal = static_cast<int>(sh.count[par]);
+    for (int i = tid; i < 256; i += blockDim.x) hist[i] = 0u;  // for pass p + 2
   }
   return {prefix, remaining, equal};
 }
@@ -183,8 +188,11 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
   float* sscore = a.state_score + static_cast<size_t>(lg) * B;
   float* pscore = a.pool_score + static_cast<size_t>(lg) * a.pool_stride;
   int32_t* ppos = a.pool_pos + static_cast<size_t>(lg) * a.pool_stride;
-  int32_t* asrc = a.admit_src + static_cast<size_t>(lg) * T;
-  int32_t* adst = a.admit_dst + static_cast<size_t>(lg) * T;
+  // admit lists (at most T entries each): in LDS for frames that fit, else the
+  // global per-(layer, KV head) lists
+  const bool lds_lists = T <= kLdsAdmit;
+  int32_t* asrc = lds_lists ? sh.admit_src : a.admit_src + static_cast<size_t>(lg) * T;
+  int32_t* adst = lds_lists ? sh.admit_dst : a.admit_dst + static_cast<size_t>(lg) * T;
 
   // Each thread sums up to kJ candidates at a time, loading kTB row tiles of
   // each before adding them, so the loads overlap instead of waiting one by one;
