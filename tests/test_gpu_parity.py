@@ -59,6 +59,8 @@ EDGE = [
     ("f32_d128_ragged", 4, 2, 128, 33, 40, 5, "f32"),
     ("bf16_d64_multi_tile", 16, 2, 64, 300, 600, 4, "bf16"),
     ("bf16_G7_T196_B300", 28, 4, 128, 196, 300, 4, "bf16"),
+    # frames over 1024 tokens: the refresh keeps its admit lists in global memory
+    ("T1100_global_admit_lists", 2, 1, 64, 1100, 1500, 3, "bf16"),
 ]
 
 
