@@ -67,16 +67,44 @@ struct RadixResult {
   int equal;       // how many active entries equal `value`
 };
 
+// Wave-wide reductions and scans in registers (DPP and lane swaps, no LDS).
+template <int CTRL>
+__device__ inline uint32_t dpp_u32(uint32_t x) {  // all rows and banks; lanes without a source read 0
+  return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, 0xF, 0xF, true));
+}
+// f over all 64 lanes (f associative and commutative), in every lane: partners
+// lane ^ 1, lane ^ 2, the mirrored quad, the mirrored half row, then the
+// other row of a pair (lanes +-16) and the other half of the wave (lanes +-32).
+template <typename F>
+__device__ inline uint32_t wave_allreduce(uint32_t x, F f) {
+  x = f(x, dpp_u32<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = f(x, dpp_u32<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = f(x, dpp_u32<0x141>(x));  // row_half_mirror
+  x = f(x, dpp_u32<0x140>(x));  // row_mirror
+  const auto r16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = f(r16[0], r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return f(r32[0], r32[1]);
+}
 __device__ inline uint32_t wave_min_u32(uint32_t x) {
-  for (int off = 32; off > 0; off >>= 1) x = min(x, static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), off, 64)));
-  return x;
+  return wave_allreduce(x, [](uint32_t a, uint32_t b) { return min(a, b); });
 }
 __device__ inline uint32_t wave_max_u32(uint32_t x) {
-  for (int off = 32; off > 0; off >>= 1) x = max(x, static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), off, 64)));
-  return x;
+  return wave_allreduce(x, [](uint32_t a, uint32_t b) { return max(a, b); });
 }
 __device__ inline int wave_sum_i32(int x) {
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return static_cast<int>(wave_allreduce(static_cast<uint32_t>(x), [](uint32_t a, uint32_t b) { return a + b; }));
+}
+// Inclusive prefix sum over lanes 0..lane: shifts by 1, 2, 4, 8 inside each row of
+// 16 lanes, then the totals of rows 0 and 2 into rows 1 and 3 (row_bcast:15) and
+// the total of rows 0-1 into rows 2 and 3 (row_bcast:31).
+__device__ inline uint32_t wave_inclusive_sum(uint32_t x) {
+  x += dpp_u32<0x111>(x);
+  x += dpp_u32<0x112>(x);
+  x += dpp_u32<0x114>(x);
+  x += dpp_u32<0x118>(x);
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x142, 0xA, 0xF, false));
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x143, 0xC, 0xF, false));
   return x;
 }
 
@@ -143,22 +171,19 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
     }
     __syncthreads();
     if (tid < 64) {
+      // lane t holds bins 255 - 4t down to 252 - 4t, so a prefix over lanes counts
+      // the keys in this lane's bins and every higher one
       uint32_t c[4];
-      for (int b = 0; b < 4; ++b) c[b] = hist[4 * tid + b];
+      for (int i = 0; i < 4; ++i) c[i] = hist[255 - 4 * tid - i];
       const uint32_t mine = c[0] + c[1] + c[2] + c[3];
-      uint32_t suffix = mine;  // sum over lanes >= tid
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t o = __shfl_down(suffix, off, 64);
-        if (tid + off < 64) suffix += o;
-      }
-      uint32_t above = suffix - mine;  // keys in higher bins
-      for (int b = 3; b >= 0; --b) {
-        if (above < static_cast<uint32_t>(remaining) && static_cast<uint32_t>(remaining) <= above + c[b]) {
-          sh.digit[par] = 4 * tid + b;
+      uint32_t above = wave_inclusive_sum(mine) - mine;  // keys in higher bins
+      for (int i = 0; i < 4; ++i) {
+        if (above < static_cast<uint32_t>(remaining) && static_cast<uint32_t>(remaining) <= above + c[i]) {
+          sh.digit[par] = 255 - 4 * tid - i;
           sh.remaining[par] = remaining - static_cast<int>(above);
-          sh.count[par] = c[b];
+          sh.count[par] = c[i];
         }
-        above += c[b];
+        above += c[i];
       }
     }
     __syncthreads();
@@ -279,7 +304,9 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
     if (j < S && !ev) sscore[j] = __uint_as_float(sbits[j]);
     int tot;
     const int rank = block_exclusive_count(ev, sh.wave_count, &tot);
-    if (ev) adst[n_ev + rank] = j;
+    // a valid selection evicts at most as many slots as it admits (<= T); only
+    // the first T can be paired, and the bound keeps the list inside its T entries
+    if (ev && n_ev + rank < T) adst[n_ev + rank] = j;
     n_ev += tot;
   }
   // Holes beyond the evicted slots are the free slots S, S+1, ... (state not yet full).
