@@ -27,26 +27,6 @@ namespace skv {
 
 namespace {
 
-// Exclusive prefix count of `flag` over the workgroup; *total receives the sum.
-__device__ inline int block_exclusive_count(bool flag, int* wave_count, int* total) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int n_waves = blockDim.x >> 6;
-  const uint64_t mask = __ballot(flag);
-  const int within = __popcll(mask & ((1ull << lane) - 1ull));
-  if (lane == 0) wave_count[wave] = __popcll(mask);
-  __syncthreads();
-  int before = 0, sum = 0;
-  for (int w = 0; w < n_waves; ++w) {
-    const int c = wave_count[w];
-    before += (w < wave) ? c : 0;
-    sum += c;
-  }
-  __syncthreads();
-  *total = sum;
-  return before + within;
-}
-
 constexpr int kLdsAdmit = 1024;  // frames up to this many tokens keep the admit lists in LDS
 
 struct SelectShared {
@@ -54,7 +34,7 @@ struct SelectShared {
   uint32_t wave_min[kSelectThreads / 64];
   uint32_t wave_max[kSelectThreads / 64];
   int wave_active[kSelectThreads / 64];
-  int wave_count[kSelectThreads / 64];  // block_exclusive_count
+  uint32_t wave_total[kSelectThreads / 64];  // admit/evict scan
   int digit[2], remaining[2];           // one slot per pass parity
   uint32_t count[2];
   int32_t admit_src[kLdsAdmit];  // frame token of the a-th admitted candidate
@@ -286,28 +266,45 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
     return kj > s_thr || (kj == s_thr && spos[j] <= p_thr);
   };
 
-  // Admitted frame tokens, ascending t.
-  int n_adm = 0;
-  for (int base = 0; base < T; base += blockDim.x) {
-    const int t = base + tid;
-    const bool adm = t < T && kept(S + t);
-    int tot;
-    const int rank = block_exclusive_count(adm, sh.wave_count, &tot);
-    if (adm) asrc[n_adm + rank] = t;
-    n_adm += tot;
+  // Admitted frame tokens (ascending t) and evicted state slots (ascending
+  // slot).  Each thread owns a contiguous chunk of both (at most 16 entries of
+  // each: S, T <= 16384 over 1024 threads); one block-wide scan of its packed
+  // counts (admitted in the low 16 bits, evicted in the high 16, totals below
+  // 2^16) gives its offsets into both lists.
+  const int nt = static_cast<int>(blockDim.x);
+  const int lane = tid & 63, wave = tid >> 6, n_waves = nt >> 6;
+  const int ca = (T + nt - 1) / nt, ce = (S + nt - 1) / nt;
+  const int a0 = tid * ca, e0 = tid * ce;
+  uint32_t adm_mask = 0u, ev_mask = 0u;
+  for (int i = 0; i < ca; ++i)
+    if (a0 + i < T && kept(S + a0 + i)) adm_mask |= 1u << i;
+  for (int i = 0; i < ce; ++i)
+    if (e0 + i < S && !kept(e0 + i)) ev_mask |= 1u << i;
+  const uint32_t mine = static_cast<uint32_t>(__popc(adm_mask)) | (static_cast<uint32_t>(__popc(ev_mask)) << 16);
+  const uint32_t incl = wave_inclusive_sum(mine);
+  if (lane == 63) sh.wave_total[wave] = incl;
+  __syncthreads();
+  uint32_t before = incl - mine, total = 0u;
+  for (int w = 0; w < n_waves; ++w) {
+    const uint32_t c = sh.wave_total[w];
+    before += w < wave ? c : 0u;
+    total += c;
   }
-  // Evicted state slots, ascending slot; retained slots get the new score.
-  int n_ev = 0;
-  for (int base = 0; base < S; base += blockDim.x) {
-    const int j = base + tid;
-    const bool ev = j < S && !kept(j);
-    if (j < S && !ev) sscore[j] = __uint_as_float(sbits[j]);
-    int tot;
-    const int rank = block_exclusive_count(ev, sh.wave_count, &tot);
-    // a valid selection evicts at most as many slots as it admits (<= T); only
-    // the first T can be paired, and the bound keeps the list inside its T entries
-    if (ev && n_ev + rank < T) adst[n_ev + rank] = j;
-    n_ev += tot;
+  const int n_adm = static_cast<int>(total & 0xFFFFu), n_ev = static_cast<int>(total >> 16);
+  int ra = static_cast<int>(before & 0xFFFFu), re = static_cast<int>(before >> 16);
+  for (int i = 0; i < ca; ++i)
+    if (adm_mask >> i & 1u) asrc[ra++] = a0 + i;
+  // retained slots get the new score; a valid selection evicts at most as many
+  // slots as it admits (<= T), and the bound keeps the list inside its T entries
+  for (int i = 0; i < ce; ++i) {
+    const int j = e0 + i;
+    if (j >= S) break;
+    if (ev_mask >> i & 1u) {
+      if (re < T) adst[re] = j;
+      ++re;
+    } else {
+      sscore[j] = __uint_as_float(sbits[j]);
+    }
   }
   // Holes beyond the evicted slots are the free slots S, S+1, ... (state not yet full).
   // Clamping keeps writes inside the B slots even for an invalid forced state
