@@ -21,9 +21,13 @@
  *   SKV_ERR_INVALID_ARG.
  * - Every device operation is enqueued on the HIP stream given to skv_init and
  *   is stream-ordered; no call blocks the host except skv_timing_stop.
- * - Errors are returned as skv_status; on error nothing is enqueued and the
- *   context is unchanged.  Asynchronous device faults surface at the caller's
- *   next synchronisation.
+ * - Errors are returned as skv_status.  Argument, order and capacity errors are
+ *   found before anything is enqueued and leave the context unchanged.  A launch
+ *   failure (SKV_ERR_DEVICE from skv_frame_step or skv_decode_step) can come
+ *   after earlier kernels of the same call were enqueued: the context is then
+ *   marked, and every later frame or decode step returns SKV_ERR_DEVICE until
+ *   skv_reset or skv_seek restarts the stream.  Asynchronous device faults
+ *   surface at the caller's next synchronisation.
  * - All device memory of a context is allocated once in skv_init and released
  *   in skv_destroy; skv_frame_step allocates nothing.
  * - A context is not thread-safe: calls on one context must be serialised.
@@ -104,6 +108,11 @@ typedef struct {
   float rope_theta;         /* RoPE base (> 0 when rope != 0), e.g. 10000 or 1e6 */
   float rope_factor;        /* YaRN scale s >= 1 (SKV_ROPE_YARN only) */
   int32_t rope_orig_max;    /* YaRN original context length (> 0, SKV_ROPE_YARN only) */
+  int32_t split_refresh;    /* 0 (a zeroed config): the refresh of a frame step is one launch (selection
+                               and state update in one set of workgroups, the decode-cache append in
+                               another); 1: three launches, selection, state update, append, so that each
+                               stage can be timed (skv_timing_*) and profiled on its own.  The results
+                               are the same bit for bit. */
 } skv_config;
 
 typedef struct skv_ctx skv_ctx;
@@ -112,7 +121,8 @@ typedef struct skv_ctx skv_ctx;
  * (compressed state and decode cache of all layers, scratch), and binds the
  * context to hip_stream (a hipStream_t; NULL means the default stream).
  * Limits: pos_offset + max_frames * T + max_decode_tokens < 2^31; B + T <= 16384
- * (STATEKV and RECENT); policy one of skv_policy, else SKV_ERR_INVALID_ARG.
+ * (STATEKV and RECENT); policy one of skv_policy and split_refresh 0 or 1, else
+ * SKV_ERR_INVALID_ARG.
  * Returns SKV_OK and *out, or an error and *out = NULL. */
 skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
 
@@ -192,26 +202,41 @@ typedef struct {
 skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* out);
 
 /* Starts a new video on the same context: frame counter, decoded-token count
- * and L_n return to 0, every state becomes empty.  Device contents are left as
- * they are (nothing is enqueued). */
+ * and L_n return to 0, every state becomes empty, and a context marked by a
+ * failed launch is usable again.  Device contents are left as they are
+ * (nothing is enqueued). */
 skv_status skv_reset(skv_ctx* ctx);
 
 /* Sets the frame counter to `frame` (0 <= frame < max_frames) at layer 0, so
  * that a caller can force a state through skv_state_view and run one step
  * from it.  The state size becomes min(B, T * frame); the decoded-token count
- * becomes 0. */
+ * becomes 0; a context marked by a failed launch is usable again. */
 skv_status skv_seek(skv_ctx* ctx, int64_t frame);
 
 /* Kernel timing with HIP events on the context's stream.  skv_timing_start
  * creates events for up to max_steps subsequent skv_frame_step or
- * skv_decode_step calls (created here, never in the step).  skv_timing_stop synchronises the stream and
- * writes ms[i * SKV_N_STAGES + s] for step i and stage s, *n_steps the number
- * of steps recorded, then releases the events.  Stages: the attention launch
- * (attention and column sums of P), and the refresh launch (score
- * finalisation, Top-B selection and state update, with the decode-cache append
- * running in the same launch).  For skv_decode_step: the split-key attention
- * with its combine, and the append. */
-enum { SKV_STAGE_ATTENTION = 0, SKV_STAGE_REFRESH = 1, SKV_N_STAGES = 2 };
+ * skv_decode_step calls (created here, never in the step).  skv_timing_stop
+ * synchronises the stream and writes ms[i * SKV_N_STAGES + s] for step i and
+ * stage s, *n_steps the number of steps recorded, then releases the events.
+ * Stages of skv_frame_step:
+ *   SKV_STAGE_ATTENTION     the attention launch(es): attention and column sums of P
+ *                           (with RoPE, the key rotation before them);
+ *   SKV_STAGE_REFRESH       the refresh launch: score finalisation, Top-B selection
+ *                           and state update, with the decode-cache append running
+ *                           in the same launch; with split_refresh, the selection
+ *                           launch only (score finalisation, Top-B, admit lists);
+ *   SKV_STAGE_STATE_UPDATE  split_refresh only: the admitted rows into their slots;
+ *   SKV_STAGE_APPEND        split_refresh only: the frame's K/V into the decode cache.
+ * Stages that a step does not run read 0.  Stages of
+ * skv_decode_step: SKV_STAGE_ATTENTION (the split-key kernel and its combine) and
+ * SKV_STAGE_APPEND (the new tokens' K/V into the decode cache). */
+enum {
+  SKV_STAGE_ATTENTION = 0,
+  SKV_STAGE_REFRESH = 1,
+  SKV_STAGE_STATE_UPDATE = 2,
+  SKV_STAGE_APPEND = 3,
+  SKV_N_STAGES = 4
+};
 skv_status skv_timing_start(skv_ctx* ctx, int32_t max_steps);
 skv_status skv_timing_stop(skv_ctx* ctx, int32_t* n_steps, float* ms, int32_t ms_capacity);
 

@@ -34,8 +34,8 @@ POLICIES = {"statekv": SKV_POLICY_STATEKV, "recent": SKV_POLICY_RECENT, "full": 
 SKV_ROPE_NONE = 0
 SKV_ROPE_PLAIN = 1
 SKV_ROPE_YARN = 2
-N_STAGES = 2
-STAGES = ("attention", "refresh")
+N_STAGES = 4
+STAGES = ("attention", "refresh", "state_update", "append")
 
 # Every symbol declared in include/statekv.h.
 EXPORTS = (
@@ -51,7 +51,7 @@ class skv_config(ctypes.Structure):
         ("max_frames", ctypes.c_int32), ("dtype", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
         ("pos_offset", ctypes.c_int64), ("policy", ctypes.c_int32), ("max_decode_tokens", ctypes.c_int32),
         ("rope", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("rope_factor", ctypes.c_float),
-        ("rope_orig_max", ctypes.c_int32),
+        ("rope_orig_max", ctypes.c_int32), ("split_refresh", ctypes.c_int32),
     ]
 
 
@@ -185,7 +185,9 @@ def skv_timing_start(ctx: int, max_steps: int) -> None:
 
 
 def skv_timing_stop(ctx: int, max_steps: int) -> np.ndarray:
-    """Per-step stage times in ms, shape [n_steps, 4] (attention, select, update, append)."""
+    """Per-step stage times in ms, shape [n_steps, N_STAGES]: attention, refresh (with
+    split_refresh: the selection launch), state update and append (split_refresh only;
+    a decode step fills attention and append)."""
     buf = (ctypes.c_float * (max_steps * N_STAGES))()
     n = ctypes.c_int32(0)
     _check(load_library().skv_timing_stop(ctypes.c_void_p(ctx), ctypes.byref(n), buf, max_steps * N_STAGES),

@@ -1,7 +1,7 @@
 // Scalar attention + importance-score kernel (fp32 arithmetic on VALU).
 //
-// Runs the fp32 configuration and serves as an independent GPU cross-check of
-// the MFMA kernel.  One wave per 64 query rows of one (layer, KV head); rows are
+// Runs the fp32 configuration (bf16 contexts use the MFMA kernel).  One wave per
+// 64 query rows of one (layer, KV head); rows are
 // the G query heads of the group times the T frame tokens.  Two sweeps over the
 // candidate keys [state slots; frame tokens] (Eq. 5):
 //   sweep 1: row maximum and sum of exp2 -> log2-sum-exp per row;
@@ -19,28 +19,17 @@ template <typename T>
 __device__ inline float load_elem(const T* p);
 template <>
 __device__ inline float load_elem<float>(const float* p) { return *p; }
-template <>
-__device__ inline float load_elem<uint16_t>(const uint16_t* p) {
-  return __uint_as_float(static_cast<uint32_t>(*p) << 16);
-}
 
 template <typename T>
 __device__ inline void store_elem(T* p, float x);
 template <>
 __device__ inline void store_elem<float>(float* p, float x) { *p = x; }
-template <>
-__device__ inline void store_elem<uint16_t>(uint16_t* p, float x) {
-  const uint32_t u = __float_as_uint(x);
-  *p = static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);  // round to nearest even
-}
 
 // A value as the storage type holds it (rotated activations are rounded to it).
 template <typename T>
 __device__ inline float round_storage(float x);
 template <>
 __device__ inline float round_storage<float>(float x) { return x; }
-template <>
-__device__ inline float round_storage<uint16_t>(float x) { return static_cast<float>(static_cast<__bf16>(x)); }
 
 constexpr int KT = 32;  // keys per LDS tile
 
@@ -149,16 +138,11 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnArgs a) {
   }
 }
 
-hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s) {
+hipError_t launch_attention_simple_f32(const AttnArgs& a, int head_dim, hipStream_t s) {
   dim3 grid((a.G * a.T + kSimpleRowsPerTile - 1) / kSimpleRowsPerTile, a.n_layers * a.H_kv);
   dim3 block(64);
-  if (bf16) {
-    if (head_dim == 64) hipLaunchKernelGGL((attn_simple_kernel<uint16_t, 64>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_simple_kernel<uint16_t, 128>), grid, block, 0, s, a);
-  } else {
-    if (head_dim == 64) hipLaunchKernelGGL((attn_simple_kernel<float, 64>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_simple_kernel<float, 128>), grid, block, 0, s, a);
-  }
+  if (head_dim == 64) hipLaunchKernelGGL((attn_simple_kernel<float, 64>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((attn_simple_kernel<float, 128>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 

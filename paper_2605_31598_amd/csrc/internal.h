@@ -62,6 +62,8 @@ struct RefreshArgs {
   int32_t* pool_pos;         // [n_layers][H_kv][pool_stride]
   int32_t* admit_src;        // [n_layers][H_kv][T]  frame token of the a-th admitted candidate
   int32_t* admit_dst;        // [n_layers][H_kv][T]  state slot it goes to
+  int32_t* admit_count;      // [n_layers][H_kv]     admitted rows (split_update only)
+  bool split_update;         // selection only: lists and count to global memory, no row copies
   void* ck;                  // [n_layers][H_kv][max_tokens][d]  decode cache
   void* cv;
   int64_t max_tokens, first_row;  // first_row = frame * T
@@ -117,9 +119,13 @@ constexpr int kMaxPool = 16384;         // B + T limit (selection keeps the pool
 
 hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attention_full_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
-hipError_t launch_attention_simple(const AttnArgs& a, int head_dim, bool bf16, hipStream_t s);
+hipError_t launch_attention_simple_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_decode_bf16(const DecodeArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s);
+// The state update and the append as launches of their own (after a launch_refresh
+// with select = true, append = false, split_update = true).
+hipError_t launch_refresh_update(const RefreshArgs& a, hipStream_t s);
+hipError_t launch_refresh_append(const RefreshArgs& a, hipStream_t s);
 // Rotates n_blocks * t key rows (t rows per (layer, KV head) block, row r at
 // relative position pos0 + r) from `in` to `out`; same layout, either dtype.
 hipError_t launch_rope_keys(const void* in, void* out, int n_blocks, int t, int row_bytes, int elem,

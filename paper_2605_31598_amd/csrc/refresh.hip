@@ -21,6 +21,9 @@
 // full attention (no compressed state) launches only these; a launch that
 // selects after an earlier append reads the frame's rows back from D.
 // Combine workgroups add the output shares of a key-split attention plan.
+// A context can also run the stages as three launches (selection with the admit
+// lists in global memory, then the state update, then the append), so that each
+// can be timed and counted on its own.
 #include "internal.h"
 
 namespace skv {
@@ -194,8 +197,9 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
   float* pscore = a.pool_score + static_cast<size_t>(lg) * a.pool_stride;
   int32_t* ppos = a.pool_pos + static_cast<size_t>(lg) * a.pool_stride;
   // admit lists (at most T entries each): in LDS for frames that fit, else the
-  // global per-(layer, KV head) lists
-  const bool lds_lists = T <= kLdsAdmit;
+  // global per-(layer, KV head) lists; a selection launch that leaves the state
+  // update to a launch of its own always writes the global lists
+  const bool lds_lists = T <= kLdsAdmit && !a.split_update;
   int32_t* asrc = lds_lists ? sh.admit_src : a.admit_src + static_cast<size_t>(lg) * T;
   int32_t* adst = lds_lists ? sh.admit_dst : a.admit_dst + static_cast<size_t>(lg) * T;
 
@@ -312,6 +316,10 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
   const int n_holes = n_ev + (B - S);
   const int count = n_adm < n_holes ? n_adm : n_holes;
   for (int i = n_ev + tid; i < count; i += blockDim.x) adst[i] = S + (i - n_ev);
+  if (a.split_update) {  // the update launch copies the rows
+    if (tid == 0) a.admit_count[lg] = count;
+    return;
+  }
   __syncthreads();  // the admit lists are read back by other threads below
 
   // State update: admitted frame rows into their slots, 16-byte chunks.
@@ -331,6 +339,37 @@ __device__ void refresh_state(const RefreshArgs& a, int lg, SelectShared& sh, ui
     if (c == 0) {
       state_pos[dst] = a.frame_pos0 + src;
       sscore[dst] = __uint_as_float(sbits[S + src]);
+    }
+  }
+}
+
+// State update of one (layer, KV head) as a launch of its own: the admitted frame
+// rows the selection launch listed (global admit lists and count) go into their
+// slots, with their position and score; the same copies as refresh_state's.
+__device__ void update_state(const RefreshArgs& a, int lg) {
+  const int tid = threadIdx.x, B = a.B, T = a.T, S = a.S;
+  const int count = a.admit_count[lg];
+  const int32_t* asrc = a.admit_src + static_cast<size_t>(lg) * T;
+  const int32_t* adst = a.admit_dst + static_cast<size_t>(lg) * T;
+  const float* pscore = a.pool_score + static_cast<size_t>(lg) * a.pool_stride;
+  int32_t* state_pos = a.state_pos + static_cast<size_t>(lg) * B;
+  float* sscore = a.state_score + static_cast<size_t>(lg) * B;
+  const int chunks = a.row_bytes >> 4;
+  const size_t src_base = static_cast<size_t>(lg) * a.kf_rows * a.row_bytes;
+  const size_t dst_base = static_cast<size_t>(lg) * B * a.row_bytes;
+  for (int idx = tid; idx < count * chunks; idx += blockDim.x) {
+    const int i = idx / chunks;
+    const int c = idx - i * chunks;
+    const int src = asrc[i], dst = adst[i];
+    const size_t so = src_base + static_cast<size_t>(src) * a.row_bytes + (static_cast<size_t>(c) << 4);
+    const size_t dof = dst_base + static_cast<size_t>(dst) * a.row_bytes + (static_cast<size_t>(c) << 4);
+    *reinterpret_cast<u32x4*>(static_cast<char*>(a.ks) + dof) =
+        *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.kf) + so);
+    *reinterpret_cast<u32x4*>(static_cast<char*>(a.vs) + dof) =
+        *reinterpret_cast<const u32x4*>(static_cast<const char*>(a.vf) + so);
+    if (c == 0) {
+      state_pos[dst] = a.frame_pos0 + src;
+      sscore[dst] = pscore[S + src];
     }
   }
 }
@@ -404,11 +443,30 @@ __global__ __launch_bounds__(kSelectThreads) void refresh_kernel(RefreshArgs a) 
   }
 }
 
+// The three stages as launches of their own (a context option for measuring each
+// stage; the results are the fused launch's, bit for bit).
+__global__ __launch_bounds__(kSelectThreads) void refresh_update_kernel(RefreshArgs a) {
+  update_state(a, static_cast<int>(blockIdx.x));
+}
+__global__ __launch_bounds__(kSelectThreads) void refresh_append_kernel(RefreshArgs a) {
+  append_frame(a, static_cast<int>(blockIdx.x));
+}
+
 hipError_t launch_refresh(const RefreshArgs& a, hipStream_t s) {
   const size_t lds = a.select ? static_cast<size_t>(a.S + a.T) * 2 * sizeof(uint32_t) : 0;
   const int grid = ((a.select ? 1 : 0) + (a.append ? 1 : 0)) * a.n_layers * a.H_kv + (a.n_ks > 1 ? a.n_comb : 0);
   if (grid == 0) return hipSuccess;
   hipLaunchKernelGGL(refresh_kernel, dim3(grid), dim3(kSelectThreads), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_refresh_update(const RefreshArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(refresh_update_kernel, dim3(a.n_layers * a.H_kv), dim3(kSelectThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_refresh_append(const RefreshArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(refresh_append_kernel, dim3(a.n_layers * a.H_kv), dim3(kSelectThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -7,6 +7,8 @@
 //      position) and the state update (admitted rows into evicted or free
 //      slots), concurrently with the decode-cache append of the frame's K/V
 //      (Eq. 4, detailed state)
+// (with skv_config.split_refresh, the refresh runs as three launches instead:
+// selection, state update, append, each timed on its own).
 // The state size S_n = min(B, n * T) and the frame's virtual positions
 // L_n + t are host-side bookkeeping (virtual sequence length paragraph), so the
 // step needs no device-to-host synchronisation.
@@ -71,6 +73,7 @@ struct skv_ctx {
   int32_t* pool_pos = nullptr;
   int32_t* admit_src = nullptr;    // [L][H_kv][T]
   int32_t* admit_dst = nullptr;
+  int32_t* admit_count = nullptr;  // [L][H_kv] (split refresh launches)
   float* rope_tab = nullptr;       // RoPE {cos, sin} per (relative position, pair), or null
   void* rope_keys = nullptr;       // with RoPE: the step's new keys, rotated: [L][H_kv][new rows][d]
   float* dec_part_o = nullptr;     // decode split partials: [dec_items][32][d]
@@ -91,6 +94,7 @@ struct skv_ctx {
   std::vector<void*> allocations;
 
   // progress of the stream
+  bool broken = false;  // a launch failed part-way through a step: steps refuse until reset/seek
   int64_t frame = 0;    // frame being processed
   int next_layer = 0;   // next layer expected within that frame
   int64_t n_decoded = 0;   // tokens decoded after the video (all layers done)
@@ -100,6 +104,7 @@ struct skv_ctx {
 
   // timing
   std::vector<hipEvent_t> events;  // (SKV_N_STAGES + 1) per recorded step
+  std::vector<uint8_t> recorded;   // per recorded step: bit i set when events[i] was recorded
   int timing_max = 0, timing_n = 0;
 };
 
@@ -282,6 +287,7 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   if (c.pos_offset + max_tokens >= (int64_t{1} << 31)) return fail(SKV_ERR_INVALID_ARG, "positions exceed int32");
   if (c.policy != SKV_POLICY_STATEKV && c.policy != SKV_POLICY_RECENT && c.policy != SKV_POLICY_FULL)
     return fail(SKV_ERR_INVALID_ARG, "unknown policy");
+  if (c.split_refresh != 0 && c.split_refresh != 1) return fail(SKV_ERR_INVALID_ARG, "split_refresh must be 0 or 1");
   const bool full = c.policy == SKV_POLICY_FULL;
   if (!full && static_cast<int64_t>(c.capacity) + c.tokens_per_frame > skv::kMaxPool)
     return fail(SKV_ERR_UNSUPPORTED, "capacity + tokens_per_frame exceeds 16384");
@@ -296,8 +302,7 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   ctx->G = c.n_q_heads / c.n_kv_heads;
   const float scale = c.softmax_scale > 0.f ? c.softmax_scale : 1.0f / std::sqrt(static_cast<float>(c.head_dim));
   ctx->scale_log2 = scale * 1.4426950408889634f;
-  const char* force_simple = std::getenv("SKV_FORCE_SIMPLE_ATTENTION");
-  ctx->use_mfma = c.dtype == SKV_BF16 && !(force_simple && force_simple[0] == '1');
+  ctx->use_mfma = c.dtype == SKV_BF16;
   ctx->tile_stride = ctx->use_mfma ? skv::plan_max_tiles(static_cast<int>(rows), skv::kMfmaRowsPerWave, skv::kMfmaWaves)
                                   : static_cast<int>((rows + skv::kSimpleRowsPerTile - 1) / skv::kSimpleRowsPerTile);
   ctx->pool_stride = ((ctx->cfg.capacity + c.tokens_per_frame + 63) / 64) * 64;
@@ -343,6 +348,7 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
       {reinterpret_cast<void**>(&ctx->pool_pos), LH * ctx->pool_stride * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_src), LH * c.tokens_per_frame * sizeof(int32_t)},
       {reinterpret_cast<void**>(&ctx->admit_dst), LH * c.tokens_per_frame * sizeof(int32_t)},
+      {reinterpret_cast<void**>(&ctx->admit_count), LH * sizeof(int32_t)},
       {&ctx->rope_keys, c.rope == SKV_ROPE_NONE ? 0 : LH * static_cast<size_t>(new_rows) * ctx->row_bytes},
       {reinterpret_cast<void**>(&ctx->dec_part_o), static_cast<size_t>(ctx->dec_items) * 32 * c.head_dim * sizeof(float)},
       {reinterpret_cast<void**>(&ctx->dec_part_ml), static_cast<size_t>(ctx->dec_items) * 64 * sizeof(float)},
@@ -382,6 +388,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   const skv_config& c = ctx->cfg;
   if (layer_count < 1 || layer_begin < 0 || layer_begin + layer_count > c.n_layers)
     return fail(SKV_ERR_INVALID_ARG, "layer range outside [0, n_layers)");
+  if (ctx->broken) return fail(SKV_ERR_DEVICE, "an earlier step failed part-way; call skv_reset or skv_seek");
   if (layer_begin != ctx->next_layer)
     return fail(SKV_ERR_ORDER, "expected layer_begin = " + std::to_string(ctx->next_layer));
   if (ctx->dec_next_layer != 0) return fail(SKV_ERR_ORDER, "a decode call is half done");
@@ -395,7 +402,15 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
 
   const bool timing = ctx->timing_n < ctx->timing_max;
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
-  auto mark = [&](int i) -> hipError_t { return timing ? hipEventRecord(ev[i], ctx->stream) : hipSuccess; };
+  uint8_t* rec = timing ? &ctx->recorded[static_cast<size_t>(ctx->timing_n)] : nullptr;
+  if (timing) *rec = 0;
+  // event i opens stage i (and closes the stage before it); a stage whose event is not
+  // recorded reads 0
+  auto mark = [&](int i) -> hipError_t {
+    if (!timing) return hipSuccess;
+    *rec |= static_cast<uint8_t>(1u << i);
+    return hipEventRecord(ev[i], ctx->stream);
+  };
 
   // with RoPE every later reader takes the frame's keys rotated (launched first below)
   const void* k_used = ctx->rope_tab != nullptr ? ctx->rope_keys : k;
@@ -454,6 +469,8 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.pool_pos = ctx->pool_pos + lh0 * ctx->pool_stride;
   ra.admit_src = ctx->admit_src + lh0 * T;
   ra.admit_dst = ctx->admit_dst + lh0 * T;
+  ra.admit_count = ctx->admit_count + lh0;
+  ra.split_update = false;
   ra.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
   ra.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
   ra.max_tokens = ctx->max_tokens;
@@ -480,7 +497,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
                               static_cast<int>(ctx->frame * T), ctx->stream);
   if (e == hipSuccess) {
     if (!ctx->use_mfma) {
-      e = skv::launch_attention_simple(aa, d, c.dtype == SKV_BF16, ctx->stream);
+      e = skv::launch_attention_simple_f32(aa, d, ctx->stream);
     } else if (full) {
       e = skv::launch_attention_full_bf16(aa, d, ctx->stream);
     } else if (plan.n_ks > 1) {  // key-split plan: statistics, output shares, their sum
@@ -493,9 +510,24 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
     }
   }
   if (e == hipSuccess) e = mark(1);
-  if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
-  if (e == hipSuccess) e = mark(2);
-  if (e != hipSuccess) return hip_fail(e, "frame step launch");
+  if (c.split_refresh) {
+    // selection (with a key-split plan's output sum), state update, append: three launches
+    skv::RefreshArgs rs = ra;
+    rs.append = false;
+    rs.split_update = true;
+    if (e == hipSuccess) e = skv::launch_refresh(rs, ctx->stream);
+    if (e == hipSuccess) e = mark(2);
+    if (e == hipSuccess && !full) e = skv::launch_refresh_update(ra, ctx->stream);
+    if (e == hipSuccess) e = mark(3);
+    if (e == hipSuccess) e = skv::launch_refresh_append(ra, ctx->stream);
+  } else {
+    if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
+  }
+  if (e == hipSuccess) e = mark(4);
+  if (e != hipSuccess) {
+    ctx->broken = true;  // earlier launches of this step may be enqueued
+    return hip_fail(e, "frame step launch");
+  }
   if (timing) ++ctx->timing_n;
 
   for (int l = layer_begin; l < layer_begin + layer_count; ++l) ctx->last_pool[l] = full ? 0 : S + T;
@@ -520,6 +552,7 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   if (n_tokens < 1 || n_tokens > skv::kDecodeMaxTokens)
     return fail(SKV_ERR_INVALID_ARG, "n_tokens must be in [1, " + std::to_string(skv::kDecodeMaxTokens) + "]");
   if (c.dtype != SKV_BF16) return fail(SKV_ERR_UNSUPPORTED, "decoding is implemented for bf16 contexts");
+  if (ctx->broken) return fail(SKV_ERR_DEVICE, "an earlier step failed part-way; call skv_reset or skv_seek");
   if (ctx->next_layer != 0) return fail(SKV_ERR_ORDER, "a frame is half done");
   if (layer_begin != ctx->dec_next_layer)
     return fail(SKV_ERR_ORDER, "expected layer_begin = " + std::to_string(ctx->dec_next_layer));
@@ -585,16 +618,27 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
 
   const bool timing = ctx->timing_n < ctx->timing_max;
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
-  auto mark = [&](int i) -> hipError_t { return timing ? hipEventRecord(ev[i], ctx->stream) : hipSuccess; };
+  uint8_t* rec = timing ? &ctx->recorded[static_cast<size_t>(ctx->timing_n)] : nullptr;
+  if (timing) *rec = 0;
+  // event i opens stage i (and closes the stage before it); a stage whose event is not
+  // recorded reads 0
+  auto mark = [&](int i) -> hipError_t {
+    if (!timing) return hipSuccess;
+    *rec |= static_cast<uint8_t>(1u << i);
+    return hipEventRecord(ev[i], ctx->stream);
+  };
   hipError_t e = mark(0);
   if (e == hipSuccess && ctx->rope_tab != nullptr)
     e = skv::launch_rope_keys(k, ctx->rope_keys, LH, t, static_cast<int>(rb), ctx->elem, ctx->rope_tab, S + n_dec,
                               ctx->stream);
   if (e == hipSuccess) e = skv::launch_decode_bf16(da, d, ctx->stream);
-  if (e == hipSuccess) e = mark(1);
+  if (e == hipSuccess) e = mark(3);
   if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
-  if (e == hipSuccess) e = mark(2);
-  if (e != hipSuccess) return hip_fail(e, "decode step launch");
+  if (e == hipSuccess) e = mark(4);
+  if (e != hipSuccess) {
+    ctx->broken = true;  // earlier launches of this step may be enqueued
+    return hip_fail(e, "decode step launch");
+  }
   if (timing) ++ctx->timing_n;
 
   ctx->dec_pending = t;
@@ -645,6 +689,7 @@ skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* 
 
 skv_status skv_reset(skv_ctx* ctx) {
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
+  ctx->broken = false;
   ctx->frame = 0;
   ctx->next_layer = 0;
   ctx->n_decoded = 0;
@@ -657,6 +702,7 @@ skv_status skv_reset(skv_ctx* ctx) {
 skv_status skv_seek(skv_ctx* ctx, int64_t frame) {
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
   if (frame < 0 || frame >= ctx->cfg.max_frames) return fail(SKV_ERR_INVALID_ARG, "frame out of range");
+  ctx->broken = false;
   ctx->frame = frame;
   ctx->next_layer = 0;
   ctx->n_decoded = 0;
@@ -669,6 +715,7 @@ skv_status skv_timing_start(skv_ctx* ctx, int32_t max_steps) {
   if (ctx == nullptr || max_steps < 1) return fail(SKV_ERR_INVALID_ARG, "bad timing request");
   for (hipEvent_t e : ctx->events) (void)hipEventDestroy(e);
   ctx->events.assign(static_cast<size_t>(max_steps) * (SKV_N_STAGES + 1), nullptr);
+  ctx->recorded.assign(static_cast<size_t>(max_steps), 0);
   for (auto& e : ctx->events) {
     const hipError_t r = hipEventCreate(&e);
     if (r != hipSuccess) {
@@ -688,10 +735,15 @@ skv_status skv_timing_stop(skv_ctx* ctx, int32_t* n_steps, float* ms, int32_t ms
   const int n = ctx->timing_n < ms_capacity / SKV_N_STAGES ? ctx->timing_n : ms_capacity / SKV_N_STAGES;
   for (int i = 0; i < n; ++i) {
     hipEvent_t* ev = &ctx->events[static_cast<size_t>(i) * (SKV_N_STAGES + 1)];
+    const unsigned rec = ctx->recorded[static_cast<size_t>(i)];
     for (int s = 0; s < SKV_N_STAGES; ++s) {
       float t = 0.f;
-      e = hipEventElapsedTime(&t, ev[s], ev[s + 1]);
-      if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+      int next = s + 1;  // the stage ends at the next recorded event
+      while (next <= SKV_N_STAGES && !(rec >> next & 1u)) ++next;
+      if ((rec >> s & 1u) && next <= SKV_N_STAGES) {
+        e = hipEventElapsedTime(&t, ev[s], ev[next]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+      }
       ms[i * SKV_N_STAGES + s] = t;
     }
   }

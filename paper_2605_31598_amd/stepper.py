@@ -19,7 +19,8 @@ class FrameStepper:
 
     def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
                  dtype="bf16", softmax_scale=0.0, pos_offset=0, stream=None, policy="statekv",
-                 max_decode_tokens=0, rope=None, rope_theta=0.0, rope_factor=1.0, rope_orig_max=0):
+                 max_decode_tokens=0, rope=None, rope_theta=0.0, rope_factor=1.0, rope_orig_max=0,
+                 split_refresh=False):
         import torch
 
         if not torch.cuda.is_available():
@@ -34,16 +35,16 @@ class FrameStepper:
         self.cfg = B.skv_config(n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
                                 _DTYPES[dtype], softmax_scale, pos_offset, B.POLICIES[policy], max_decode_tokens,
                                 {None: B.SKV_ROPE_NONE, "plain": B.SKV_ROPE_PLAIN, "yarn": B.SKV_ROPE_YARN}[rope],
-                                rope_theta, rope_factor, rope_orig_max)
+                                rope_theta, rope_factor, rope_orig_max, int(bool(split_refresh)))
         self.n_layers, self.H_q, self.H_kv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         # streaming full attention keeps no compressed state
         self.T, self.B, self.max_frames = tokens_per_frame, (0 if policy == "full" else capacity), max_frames
         self.ctx = B.skv_init(self.cfg, self.stream.cuda_stream)
 
     @classmethod
-    def from_workload(cls, wl, max_frames=None, stream=None, policy="statekv", max_decode_tokens=0, **rope):
+    def from_workload(cls, wl, max_frames=None, stream=None, policy="statekv", max_decode_tokens=0, **kw):
         return cls(wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.tokens_per_frame, wl.capacity,
-                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream, policy, max_decode_tokens, **rope)
+                   max_frames or wl.n_frames, wl.dtype, 0.0, wl.pos_offset, stream, policy, max_decode_tokens, **kw)
 
     # ------------------------------------------------------------------ step
     def _check(self, name, t, heads, n_layers):
@@ -143,6 +144,23 @@ class FrameStepper:
             arr = np.empty((H, n, d), dtype=self.np_dtype)
             for g in range(H):
                 arr[g] = B.copy_to_host(base + g * M * d * self.elem, n * d * self.elem).view(self.np_dtype).reshape(n, d)
+            out.append(arr)
+        return out[0], out[1], cv.n_tokens
+
+    def read_cache_rows(self, layer, r0, r1):
+        """Host copy of decode-cache rows [r0, r1) of every KV head: (k, v) [H_kv, r1 - r0, d]
+        and the number of video rows the layer has written."""
+        self._sync()
+        cv = B.skv_decode_cache_view(self.ctx, layer)
+        H, d, M, n = self.H_kv, self.d, cv.max_tokens, r1 - r0
+        if not 0 <= r0 <= r1 <= M:
+            raise ValueError(f"rows [{r0}, {r1}) outside the cache's {M} rows")
+        out = []
+        for base in (cv.k, cv.v):
+            arr = np.empty((H, n, d), dtype=self.np_dtype)
+            for g in range(H):
+                arr[g] = B.copy_to_host(base + (g * M + r0) * d * self.elem, n * d * self.elem).view(
+                    self.np_dtype).reshape(n, d)
             out.append(arr)
         return out[0], out[1], cv.n_tokens
 

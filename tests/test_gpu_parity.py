@@ -17,7 +17,8 @@ from workloads import CONFIGS, WorkloadConfig  # noqa: E402
 from workloads import generate as gen  # noqa: E402
 
 from .gpu_harness import (  # noqa: E402
-    compare_step, frame_tensors, gpu_state_as_oracle, oracle_step, recent_state, run_tracking, say, to_device,
+    NEAR_TIE_REL, compare_step, frame_tensors, gpu_state_as_oracle, oracle_step, recent_state, run_tracking, say,
+    to_device,
 )
 
 
@@ -29,8 +30,16 @@ def _gpu():
 
 
 # --------------------------------------------------------------------------
-# whole videos, every frame checked on the GPU's own state + independent run
+# whole videos, end to end: the GPU's state evolves by itself from the empty
+# state; every frame is checked against the oracle, and every frame where the
+# GPU keeps another set than the oracle's own evolution must be a near-tie
 # --------------------------------------------------------------------------
+def _assert_divergences_at_near_ties(s):
+    assert len(s["divergences"]) == s["near_tie_diffs"]
+    for d in s["divergences"]:
+        assert d["gap"] <= NEAR_TIE_REL, f"divergence away from a near-tie: {d}"
+
+
 def test_tiny_f32_whole_video():
     wl = CONFIGS["tiny_f32"]
     s = run_tracking(wl, wl.n_frames, [0])
@@ -43,6 +52,37 @@ def test_vlm7b_1layer_whole_video():
     wl = CONFIGS["vlm7b_1layer"]
     s = run_tracking(wl, wl.n_frames, [0], log_every=8)
     say(f"vlm7b_1layer: {s}")
+    _assert_divergences_at_near_ties(s)
+
+
+def test_vlm7b_28layer_whole_video():
+    """All 512 frames of the 7B stack, all 28 layers per call as the benchmark runs
+    them; layers 0 and 27 checked every frame (the others get zero inputs)."""
+    wl = CONFIGS["vlm7b_28layer"]
+    s = run_tracking(wl, wl.n_frames, [0, 27], log_every=32)
+    _assert_divergences_at_near_ties(s)
+    s["divergences"] = s["divergences"][:8]
+    say(f"vlm7b_28layer whole video: {s}")
+
+
+def test_vlm72b_80layer_stream_past_state_full():
+    """The 72B stack from the empty state through 64 frames past state-full (frame 16),
+    all 80 layers per call; layers 0 and 79 checked every frame."""
+    wl = CONFIGS["vlm72b_80layer"]
+    n = wl.full_from_frame + 64
+    s = run_tracking(wl, n, [0, 79], log_every=8)
+    say(f"vlm72b_80layer frames 0..{n - 1}: {s}")
+    _assert_divergences_at_near_ties(s)
+
+
+def test_stress_stream_past_state_full():
+    """The stress layer (duplicate and heavy keys) from the empty state through 64 frames
+    past state-full (frame 12)."""
+    wl = CONFIGS["stress_1layer"]
+    n = wl.full_from_frame + 64
+    s = run_tracking(wl, n, [0], log_every=8)
+    say(f"stress_1layer frames 0..{n - 1}: {s}")
+    _assert_divergences_at_near_ties(s)
 
 
 # --------------------------------------------------------------------------
@@ -102,8 +142,11 @@ FULL = [("vlm7b_28layer", [0, 13, 27], 40), ("vlm72b_80layer", [0, 79], 20), ("s
 def test_full_size_one_frame_on_forced_full_state(name, layers, frame):
     wl = CONFIGS[name]
     forced = {l: recent_state(wl, l, frame) for l in layers}
-    s = run_tracking(wl, 1, layers, start_frame=frame, forced=forced, independent=False)
+    s = run_tracking(wl, 1, layers, start_frame=frame, forced=forced)
     say(f"{name} frame {frame}: {s}")
+    if name == "stress_1layer":
+        # duplicate keys tie exactly across the capacity boundary: the tie pass decides
+        assert s["straddle_oracle"] >= 1 and s["straddle_gpu"] >= 1
 
 
 PER_LAYER = [("vlm7b_28layer", [0, 27], 40), ("vlm72b_80layer", [0, 79], 20)]
@@ -115,22 +158,56 @@ def test_full_size_one_layer_per_call_on_forced_full_state(name, layers, frame):
     fill the device, so the attention splits the keys over 10 (7B) or 4 (72B) ranges."""
     wl = CONFIGS[name]
     forced = {l: recent_state(wl, l, frame) for l in layers}
-    s = run_tracking(wl, 2, layers, start_frame=frame, forced=forced, independent=False, per_layer=True)
+    s = run_tracking(wl, 2, layers, start_frame=frame, forced=forced, per_layer=True)
     say(f"{name} frames {frame}-{frame + 1}, one layer per call: {s}")
 
 
-def test_vlm7b_28layer_stream_through_state_full():
-    """First 14 frames of the 28-layer stack (state full from frame 11), layers 0 and 27 checked."""
-    wl = CONFIGS["vlm7b_28layer"]
-    s = run_tracking(wl, 14, [0, 27], log_every=2)
-    say(f"vlm7b_28layer 14 frames: {s}")
-
-
 def test_stress_ties_resolved_by_position():
-    """Stress keys: exact duplicate rows inside the state give bit-equal GPU scores; the lower position wins."""
+    """Stress keys on the most recent state entering frame 15: exact duplicate rows give
+    bit-equal scores on both sides, and in at least one KV head the tied entries straddle
+    the capacity boundary (kv head 7: 26 tied scores for 14 places), so the lowest
+    positions must win."""
     wl = CONFIGS["stress_1layer"].with_(n_frames=16)
-    s = run_tracking(wl, 2, [0], start_frame=14, forced={0: recent_state(wl, 0, 14)}, independent=False)
-    say(f"stress: {s}")
+    s = run_tracking(wl, 1, [0], start_frame=15, forced={0: recent_state(wl, 0, 15)})
+    say(f"stress frame 15: {s}")
+    assert s["straddle_oracle"] >= 1, "the oracle's pool has no tie across the boundary"
+    assert s["straddle_gpu"] >= 1, "the GPU's pool has no tie across the boundary"
+
+
+@pytest.mark.parametrize("Hq,Hkv,d,T,B,N", [(8, 2, 128, 40, 100, 6), (28, 4, 128, 196, 2048, 13)],
+                         ids=["small", "vlm7b_layer"])
+def test_zero_queries_keep_the_earliest_tokens(Hq, Hkv, d, T, B, N):
+    """Q = 0: attention is uniform, every state key and frame token 0 tie exactly (on
+    the GPU too: equal logits give equal exponentials summed in the same order), so
+    once the state is full B + 1 entries tie for B places and the tie rule keeps the
+    earliest B tokens forever (closed form of the selection)."""
+    wl = WorkloadConfig("zero_q", 1, Hq, Hkv, d, T, N, B, "bf16", "iid", 5150, pos_offset=7)
+    st = FrameStepper.from_workload(wl)
+    own = orc.LayerState.empty(Hkv, d)
+    straddle = 0
+    try:
+        out = torch.empty((1, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+        for n in range(N):
+            x = gen.frame_inputs(wl, 0, n)
+            x["q"] = np.zeros_like(x["q"])
+            st.step(to_device(x["q"][None], "bf16"), to_device(x["k"][None], "bf16"),
+                    to_device(x["v"][None], "bf16"), out)
+            res = oracle_step(wl, own, x, n)
+            after = st.read_state(0)
+            rep = compare_step(res, out[0].float().cpu().numpy().astype(np.float64), after["pool_score"],
+                               after["pool_pos"], after["pos"], B, "bf16", f"zero_q frame {n}")
+            assert rep["near_tie_diffs"] == 0
+            seen = (n + 1) * T
+            earliest = wl.pos_offset + np.arange(min(B, seen))
+            for g in range(Hkv):
+                assert np.array_equal(np.sort(after["pos"][g]), earliest), f"frame {n} kv head {g}"
+            if n >= wl.full_from_frame:
+                assert rep["straddle_gpu"] == Hkv and rep["straddle_oracle"] == Hkv, rep
+            straddle += rep["straddle_gpu"]
+            own = gpu_state_as_oracle(after, "bf16")
+    finally:
+        st.close()
+    say(f"zero_q {Hq}/{Hkv} T={T} B={B}: straddling ties on the GPU in {straddle} head-frames")
 
 
 # --------------------------------------------------------------------------
@@ -213,3 +290,63 @@ def test_device_lowrank_keys_match_host():
         got = out.view(torch.int16).cpu().numpy().view(np.uint16)
         for i, f in enumerate(frames):
             assert np.array_equal(got[i], gen.frame_inputs(wl, layer, f)["k"]), (layer, f)
+
+
+def test_device_stress_keys_match_host():
+    """The stress layer's keys (templates and heavy rows), built on the device for the
+    benchmark, equal the host generator's."""
+    from workloads import device
+
+    wl = CONFIGS["stress_1layer"]
+    frames = [0, 13, 1023]
+    out = torch.empty((len(frames), wl.n_kv_heads, wl.tokens_per_frame, wl.head_dim), dtype=torch.bfloat16,
+                      device="cuda")
+    device.fill_stress_keys(out, wl, 0, frames)
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    for i, f in enumerate(frames):
+        assert np.array_equal(got[i], gen.frame_inputs(wl, 0, f)["k"]), f
+
+
+SPLIT = [
+    # name, layers, H_q, H_kv, d, T, B, N, policy
+    ("vlm7b_1layer_key_split", 1, 28, 4, 128, 196, 1024, 8, "statekv"),
+    ("two_layers_recent", 2, 8, 2, 128, 48, 100, 5, "recent"),
+    ("T1100_global_lists", 1, 2, 1, 64, 1100, 1500, 3, "statekv"),
+    ("capacity0", 2, 8, 2, 64, 24, 0, 3, "statekv"),
+    ("full_policy", 2, 8, 2, 128, 40, 64, 4, "full"),
+]
+
+
+@pytest.mark.parametrize("name,L,Hq,Hkv,d,T,B,N,policy", SPLIT, ids=[x[0] for x in SPLIT])
+def test_split_refresh_launches_match_the_fused_launch(name, L, Hq, Hkv, d, T, B, N, policy):
+    """The refresh as three launches (selection, state update, append) gives the fused
+    launch's outputs, states, pool scores and decode cache bit for bit; its stage timings
+    are filled, the fused context's update and append stages read 0."""
+    wl = WorkloadConfig(name, L, Hq, Hkv, d, T, N, B, "bf16", "iid", 31337, pos_offset=5)
+    a = FrameStepper.from_workload(wl, policy=policy)
+    b = FrameStepper.from_workload(wl, policy=policy, split_refresh=True)
+    try:
+        oa = torch.empty((L, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+        ob = torch.empty_like(oa)
+        a.timing_start(N)
+        b.timing_start(N)
+        for n in range(N):
+            q, k, v, _ = frame_tensors(wl, n, list(range(L)))
+            a.step(q, k, v, oa)
+            b.step(q, k, v, ob)
+            assert torch.equal(oa.view(torch.int16), ob.view(torch.int16)), f"output, frame {n}"
+            for l in range(L):
+                sa, sb = a.read_state(l), b.read_state(l)
+                for key in ("pos", "score", "k", "v", "pool_score", "pool_pos"):
+                    assert np.array_equal(sa[key], sb[key]), f"{key}, layer {l} frame {n}"
+        ta, tb = a.timing_stop(N), b.timing_stop(N)
+        assert np.all(ta[:, 2:] == 0.0) and np.all(ta[:, 0] > 0.0)
+        assert np.all(tb[:, 3] > 0.0) and np.all(tb[:, 0] > 0.0)
+        if policy != "full":
+            assert np.all(tb[:, 1] > 0.0) and np.all(tb[:, 2] > 0.0)
+        for l in range(L):
+            ca, cb = a.read_cache(l), b.read_cache(l)
+            assert np.array_equal(ca[0], cb[0]) and np.array_equal(ca[1], cb[1]) and ca[2] == cb[2] == N * T
+    finally:
+        a.close()
+        b.close()

@@ -298,6 +298,32 @@ def test_yarn_reduces_to_rope_and_blends_by_wavelength():
     check_yarn_limits()
 
 
+def check_yarn_ramp_interior():
+    """YaRN's ramp between its limits: two pairs whose wavelength ratio lies strictly inside
+    (1, 32), against values worked by hand from YaRN's definition
+    (tests/golden/yarn_ramp_interior.json holds the derivation)."""
+    import json
+
+    g = json.load(open(os.path.join(HERE, "golden", "yarn_ramp_interior.json")))
+    c = g["config"]
+    spec = orc.rope_spec(c["head_dim"], c["theta"], "yarn", factor=c["factor"], orig_max=c["orig_max"], dtype="f32")
+    np.testing.assert_allclose(spec.freqs, g["expect_freqs"], rtol=1e-12)
+    assert abs(spec.mscale - g["expect_mscale"]) <= 1e-12
+    d, half, p = c["head_dim"], c["head_dim"] // 2, g["rotation_position"]
+    for j, (cos_m, sin_m) in g["expect_rotated_unit"].items():
+        j = int(j)
+        x = np.zeros((1, d))
+        x[0, j] = 1.0
+        y = orc.rope_rotate(x, np.array([p]), spec)[0]
+        np.testing.assert_allclose([y[j], y[j + half]], [cos_m, sin_m], rtol=2e-7)  # rounded to fp32
+        others = np.delete(y, [j, j + half])
+        assert np.all(others == 0.0)
+
+
+def test_yarn_ramp_interior_hand_worked():
+    check_yarn_ramp_interior()
+
+
 def test_rope_bf16_rounding_matches_a_library_conversion():
     x = np.random.default_rng(3).standard_normal(4096) * 10.0 ** np.random.default_rng(4).uniform(-3, 3, 4096)
     ref = torch.from_numpy(x).to(torch.bfloat16).double().numpy()
@@ -503,6 +529,32 @@ def _mut_rope_clockwise(x, positions, spec):
     return _ROPE(x, -np.asarray(positions, dtype=np.float64), spec)  # wrong direction
 
 
+_SPEC = orc.rope_spec
+
+
+def _yarn_variant(head_dim, theta, kind, factor, orig_max, dtype, beta=32.0, invert=False, temperature=True):
+    if kind != "yarn":
+        return _SPEC(head_dim, theta, kind, factor, orig_max, dtype)
+    j = np.arange(head_dim // 2, dtype=np.float64)
+    f = theta ** (-2.0 * j / head_dim)
+    g = np.clip((orig_max * f / (2.0 * np.pi) - 1.0) / (beta - 1.0), 0.0, 1.0)
+    if invert:
+        g = 1.0 - g
+    return orc.RopeSpec((1.0 - g) * f / factor + g * f, 0.1 * np.log(factor) + 1.0 if temperature else 1.0, dtype)
+
+
+def _mut_yarn_beta(head_dim, theta, kind="plain", factor=1.0, orig_max=0, dtype="bf16"):
+    return _yarn_variant(head_dim, theta, kind, factor, orig_max, dtype, beta=64.0)  # wrong ramp edge
+
+
+def _mut_yarn_inverted(head_dim, theta, kind="plain", factor=1.0, orig_max=0, dtype="bf16"):
+    return _yarn_variant(head_dim, theta, kind, factor, orig_max, dtype, invert=True)  # interpolates the wrong end
+
+
+def _mut_yarn_no_temperature(head_dim, theta, kind="plain", factor=1.0, orig_max=0, dtype="bf16"):
+    return _yarn_variant(head_dim, theta, kind, factor, orig_max, dtype, temperature=False)
+
+
 def _mut_recent_oldest(pos, capacity):
     P = pos.shape[0]
     keep = np.arange(P) if P <= capacity else np.argsort(pos, kind="stable")[:capacity]  # wrong: oldest
@@ -514,7 +566,7 @@ PINS = [check_golden, check_full_capacity_is_causal_sdpa,
         check_zero_capacity_is_framewise_sdpa, check_zero_query_closed_form,
         lambda: check_bruteforce(1, 4, 2, 4, 4, 3, 4, 5), check_full_policy_is_causal_sdpa,
         check_recent_policy_window, check_decode_is_causal_sdpa, check_rope_closed_form,
-        check_rope_relative_positions]
+        check_rope_relative_positions, check_yarn_limits, check_yarn_ramp_interior]
 
 
 @pytest.mark.parametrize("name,attr,mutant", [
@@ -529,6 +581,9 @@ PINS = [check_golden, check_full_capacity_is_causal_sdpa,
     ("recency window keeps the oldest", "select_recent", _mut_recent_oldest),
     ("RoPE pairs adjacent dimensions", "rope_rotate", _mut_rope_interleaved),
     ("RoPE rotates clockwise", "rope_rotate", _mut_rope_clockwise),
+    ("YaRN ramp upper edge 64", "rope_spec", _mut_yarn_beta),
+    ("YaRN ramp inverted", "rope_spec", _mut_yarn_inverted),
+    ("YaRN without temperature", "rope_spec", _mut_yarn_no_temperature),
 ])
 def test_planted_mistake_is_caught(monkeypatch, name, attr, mutant):
     monkeypatch.setattr(orc, attr, mutant)

@@ -167,3 +167,64 @@ def test_key_splits_for_one_layer_of_the_7b_stack(planner):
     # the whole 28-layer stack fills the device without splitting keys
     _, n_ks, _, _ = planner(28 * 4, 7 * 196, 8, 32, True, 16, with_ks=True)
     assert n_ks == 1
+
+
+SWEEP = r'''
+#include <cstdio>
+#include <vector>
+#include "plan.h"
+// Sweeps many shapes through the planner under AddressSanitizer and
+// UndefinedBehaviorSanitizer, checking that every query row of every
+// (layer, KV head) is covered exactly once per key split and that tile slots
+// stay under plan_max_tiles.
+int main() {
+  const int rows_list[] = {1, 5, 31, 32, 33, 196, 255, 256, 257, 1372, 2048, 2916, 5000};
+  long checked = 0;
+  for (int n_lg : {1, 2, 3, 4, 7, 8, 16, 28, 112, 640})
+    for (int rows : rows_list)
+      for (int n_xcd : {1, 8})
+        for (int cu : {1, 4, 32})
+          for (int split_short : {0, 1})
+            for (int max_ks : {1, 16}) {
+              const skv::AttnPlan p = skv::plan_attention(n_lg, rows, 32, 8, n_xcd, cu, split_short != 0, max_ks);
+              const int bound = skv::plan_max_tiles(rows, 32, 8);
+              std::vector<int> cover(static_cast<size_t>(n_lg) * rows * p.n_ks, 0);
+              for (const auto& w : p.items) {
+                if (w.rows <= 0) continue;
+                if (w.lg < 0 || w.lg >= n_lg || w.row0 < 0 || w.row0 + w.rows > rows || w.tile < 0 ||
+                    w.tile >= bound || w.ks < 0 || w.ks >= p.n_ks) {
+                  printf("bad item lg=%d row0=%d rows=%d tile=%d ks=%d\n", w.lg, w.row0, w.rows, w.tile, w.ks);
+                  return 1;
+                }
+                for (int r = w.row0; r < w.row0 + w.rows; ++r)
+                  ++cover[(static_cast<size_t>(w.lg) * p.n_ks + w.ks) * rows + r];
+              }
+              for (int c : cover)
+                if (c != 1) {
+                  printf("row covered %d times (n_lg=%d rows=%d)\n", c, n_lg, rows);
+                  return 1;
+                }
+              if (static_cast<int>(p.tiles.size()) != n_lg) return 1;
+              for (int t : p.tiles)
+                if (t < 1 || t > bound) return 1;
+              ++checked;
+            }
+  printf("checked %ld plans\n", checked);
+  return 0;
+}
+'''
+
+
+def test_planner_under_address_and_undefined_behaviour_sanitizers(tmp_path):
+    """The planner built with -fsanitize=address,undefined (host code only) over a sweep
+    of shapes: no out-of-bounds access, overflow or other undefined behaviour, and every
+    row covered once per key split."""
+    src = tmp_path / "sweep.cpp"
+    src.write_text(SWEEP)
+    exe = tmp_path / "sweep"
+    subprocess.run(["g++", "-O1", "-g", "-std=c++17", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                    "-fno-omit-frame-pointer", "-I", CSRC, str(src), os.path.join(CSRC, "plan.cpp"), "-o", str(exe)],
+                   check=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, env={**os.environ, "ASAN_OPTIONS": "detect_leaks=1"})
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "checked" in r.stdout
