@@ -3,14 +3,16 @@
 A step is one frame of the video through every layer of the stack (attention
 with fused importance scoring, Top-B selection, state update, decode-cache
 append), in one skv_frame_step call.  The whole 512-frame video's Q/K/V are
-generated on the device and resident in HBM before timing; after the last
-frame the stream restarts from frame 0 with an empty state (skv_reset).
+generated on the device and resident in HBM before timing.  Every warm-up and
+timed step is a state-full frame (frames 11..511 of a 512-frame video): as many
+video streams as the W + K steps need are filled to state-full first, untimed,
+and then stepped through their remaining frames one after another.
 
 Reported: frames/s over the K timed frames (host wall clock between two
 device synchronisations), per-stage kernel times from HIP events recorded on
-the library's stream, the attention kernel's roofline position, per-frame
-latency against frame index, and the fp64 CPU oracle timed on a bounded
-sample of the same workload.
+the library's stream, the attention kernel's roofline position, the per-frame
+latency of whole videos against frame index, and the fp64 CPU oracle timed on
+a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -94,6 +96,20 @@ def refresh_bytes(wl, S, n_qtiles, admitted):
     return select + update + append
 
 
+def refresh_stage_bytes(wl, S, n_qtiles, admitted):
+    """refresh_bytes split by stage: "select" (score finalisation and Top-B: column-sum
+    partials and state positions read; pool scores/positions, retained slot scores and
+    the admit lists written), "update" (admit lists and the admitted rows' scores read,
+    the admitted K/V rows read and written with position and score) and "append" (the
+    frame's K/V read and written to the decode cache)."""
+    LH = wl.n_layers * wl.n_kv_heads
+    T, rb = wl.tokens_per_frame, wl.head_dim * 2
+    P = S + T
+    return {"select": LH * (n_qtiles * P * 4 + S * 4 + P * 8 + S * 4 + 2 * admitted * 4),
+            "update": LH * admitted * (2 * 4 + 4 + 2 * 2 * rb + 8),
+            "append": LH * T * rb * 2 * 2}
+
+
 def full_attention_flops(wl, n):
     """Causal-exact FLOPs of frame n under streaming full attention (all n*T earlier tokens)."""
     return attention_flops(wl, n * wl.tokens_per_frame)
@@ -103,7 +119,8 @@ def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
     """The paper's two comparison systems on the same resident inputs, outside the timed
     region of the main line: streaming full attention over the decode cache (one whole
     video, per-frame times) and the recency window of B tokens (one video); and StateKV
-    with YaRN-scaled RoPE applied inside the step at virtual positions (one video)."""
+    with YaRN-scaled RoPE applied inside the step at virtual positions (one video).  Each
+    video starts on a busy device (Heater); its time is the GPU's elapsed time."""
     from paper_2605_31598_amd import FrameStepper
     import torch
 
@@ -111,21 +128,15 @@ def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
     res = {}
     runs = {"full": dict(policy="full"), "recent": dict(policy="recent"),
             "statekv_yarn": dict(policy="statekv", rope="yarn", rope_theta=1e6, rope_factor=4.0, rope_orig_max=32768)}
+    heater = Heater(wl, q_all, k_all, v_all, out, stream)
     for name, kw in runs.items():
         policy = kw["policy"]
         st = FrameStepper.from_workload(wl, stream=stream, **kw)
         try:
-            for f in range(4):  # warm the kernels, then restart the stream
+            for f in range(4):  # warm the kernels; the video below restarts the stream
                 st.step(q_all[f], k_all[f], v_all[f], out)
-            st.reset()
-            torch.cuda.synchronize()
-            st.timing_start(N)
-            t0 = time.perf_counter()
-            for f in range(N):
-                st.step(q_all[f], k_all[f], v_all[f], out)
-            torch.cuda.synchronize()
-            wall = time.perf_counter() - t0
-            ms = st.timing_stop(N).astype(np.float64)
+            ms3, secs = timed_videos(st, heater, q_all, k_all, v_all, out, 1, 96)
+            ms, wall = ms3[0], float(secs[0])
         finally:
             st.close()
         frame_ms = ms.sum(axis=1)
@@ -142,6 +153,7 @@ def baselines(wl, q_all, k_all, v_all, out, stream, statekv_ms):
             entry["statekv_speedup_at_last_frame"] = round(float(frame_ms[-1] / statekv_ms), 2)
         res[name] = entry
         print(f"[bench] {name}: {entry['frames_per_s']} frames/s over one video", file=sys.stderr, flush=True)
+    heater.close()
     res["statekv_frame_ms_state_full"] = round(statekv_ms, 4)
     return res
 
@@ -217,7 +229,7 @@ def decode_bench(wl, q_all, k_all, v_all, out, stream, n_calls=32):
             "cached_tokens_per_kv_head": int(N * T), "calls": n_calls,
             "ms_per_call": round(float(att.mean()), 4), "tokens_per_s": round(n_calls / wall, 1),
             "kv_bytes_per_call": float(kv_bytes.mean()), "GBps": round(gbs, 1), "peak_GBps": PEAK_HBM_GBS,
-            "frac": round(gbs / PEAK_HBM_GBS, 4), "append_ms_per_call": round(float(ms[:, 1].mean()), 4)}
+            "frac": round(gbs / PEAK_HBM_GBS, 4), "append_ms_per_call": round(float(ms[:, 3].mean()), 4)}
 
 
 def per_layer_bench(wl, q_all, k_all, v_all, out, stream, n_frames=16):
@@ -383,17 +395,265 @@ def cpu_baseline(wl, seconds):
     }
 
 
+def curve_summary(ms, full_from, every=16):
+    """Per-frame times [videos, N] (ms) -> the per-frame median over the videos, its
+    state-full median, flatness (largest relative deviation of a state-full frame from
+    that median) and the curve decimated for the JSON line."""
+    med = np.median(ms, axis=0)
+    N = med.shape[0]
+    sf = med[full_from:]
+    m = float(np.median(sf))
+    keep = sorted(set(range(min(full_from + 4, N))) | set(range(0, N, every)) | {N - 1})
+    return {"frame_ms_median_state_full": round(m, 4),
+            "flatness_max_dev": round(float(np.max(np.abs(sf / m - 1.0))), 4),
+            "flatness_frames": [int(full_from), int(N - 1)],
+            "frame_ms_by_frame": {str(f): round(float(med[f]), 4) for f in keep}}
+
+
+class Heater:
+    """A second video stream of the same workload that keeps the device busy: creating the
+    timing events of a measured run takes the host tens of milliseconds, during which the
+    GPU idles and lowers its clock, and the clock needs about as long again to come back.
+    heat(n) enqueues n more frames of this stream (cycling through its video) without
+    waiting, so the measured frames that follow start on a busy device."""
+
+    def __init__(self, wl, q, k, v, out, stream):
+        from paper_2605_31598_amd import FrameStepper
+
+        self.st = FrameStepper.from_workload(wl, stream=stream)
+        self.q, self.k, self.v, self.out, self.N = q, k, v, out, wl.n_frames
+        self.f = 0
+
+    def heat(self, n):
+        for _ in range(n):
+            if self.f == self.N:
+                self.st.reset()
+                self.f = 0
+            self.st.step(self.q[self.f], self.k[self.f], self.v[self.f], self.out)
+            self.f += 1
+
+    def close(self):
+        self.st.close()
+
+
+def timed_videos(st, heater, q, k, v, out, n_videos, heat_frames):
+    """n_videos whole videos on stream st from the empty state, each with per-frame HIP events
+    (created before the heater's frames) and a GPU-side elapsed time over the whole video.
+    Returns per-frame stage times [videos, N, stages] and the videos' elapsed seconds."""
+    import torch
+
+    N = q.shape[0]
+    ms, secs = [], []
+    for _ in range(n_videos):
+        st.reset()
+        st.timing_start(N)
+        heater.heat(heat_frames)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for f in range(N):
+            st.step(q[f], k[f], v[f], out)
+        b.record()
+        b.synchronize()
+        secs.append(a.elapsed_time(b) * 1e-3)
+        ms.append(st.timing_stop(N).astype(np.float64))
+    return np.stack(ms), np.array(secs)
+
+
+def video_curve(wl, q_all, k_all, v_all, out, stream, n_videos=3, heat_frames=96):
+    """Whole 512-frame videos with per-frame HIP events (frame time = attention + refresh):
+    one untimed warm-up video, then n_videos videos from the empty state (skv_reset
+    between), each started on a busy device (Heater).  Reports whole-video frames/s (GPU
+    elapsed time over each video, and over the summed per-frame event times), the
+    per-frame curve of the attention and refresh launches and its flatness from state-full
+    on; `idle_start` repeats one video started right after the event creation, without
+    the heater, for comparison."""
+    from paper_2605_31598_amd import FrameStepper
+
+    N = wl.n_frames
+    st = FrameStepper.from_workload(wl, stream=stream)
+    heater = Heater(wl, q_all, k_all, v_all, out, stream)
+    try:
+        for f in range(N):  # warm-up video
+            st.step(q_all[f], k_all[f], v_all[f], out)
+        ms, secs = timed_videos(st, heater, q_all, k_all, v_all, out, n_videos, heat_frames)
+        idle_ms, idle_secs = timed_videos(st, heater, q_all, k_all, v_all, out, 1, 0)
+    finally:
+        heater.close()
+        st.close()
+    frame = ms.sum(axis=2)
+    res = {"videos": n_videos, "frames_per_video": N,
+           "frames_per_s": round(float(np.median(N / secs)), 2),
+           "frames_per_s_events": round(float(np.median(N / (frame.sum(axis=1) * 1e-3))), 2)}
+    res.update(curve_summary(frame, wl.full_from_frame))
+    full = wl.full_from_frame
+    res["attention_ms_state_full"] = round(float(np.median(ms[:, full:, 0])), 4)
+    res["refresh_ms_state_full"] = round(float(np.median(ms[:, full:, 1:].sum(axis=2))), 4)
+    idle = idle_ms.sum(axis=2)[0]
+    res["idle_start"] = {"frames_per_s": round(float(N / idle_secs[0]), 2),
+                         "frame_ms_at": {str(f): round(float(idle[f]), 4) for f in (full, full + 16, 64, 128, N - 1)},
+                         "flatness_max_dev": curve_summary(idle[None], full)["flatness_max_dev"]}
+    print(f"[bench] {wl.name}: whole videos {res['frames_per_s']} frames/s, flatness "
+          f"{res['flatness_max_dev']} (idle start {res['idle_start']['flatness_max_dev']})", file=sys.stderr,
+          flush=True)
+    return res
+
+
+def single_layer_line(name, stream, n_videos=3, heat_frames=256):
+    """A one-layer workload as its own line: the whole video resident in HBM (generated on
+    the device), one warm-up video, then n_videos whole videos with per-frame events, each
+    started on a busy device (Heater); attention TFLOP/s (algorithmic and executed MFMA
+    work) over the state-full frames."""
+    from paper_2605_31598_amd import FrameStepper
+    from workloads import CONFIGS
+    from workloads import device as wdev
+    from workloads import generate as gen
+    import torch
+
+    wl = CONFIGS[name]
+    N, Hq, Hkv, T, d = wl.n_frames, wl.n_q_heads, wl.n_kv_heads, wl.tokens_per_frame, wl.head_dim
+    q = torch.empty((N, 1, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    k = torch.empty((N, 1, Hkv, T, d), dtype=torch.bfloat16, device="cuda")
+    v = torch.empty_like(k)
+    wdev.fill_iid(q, [gen.stream_key(wl.seed, 0, f, gen.TENSOR_Q) for f in range(N)], "bf16")
+    wdev.fill_iid(v, [gen.stream_key(wl.seed, 0, f, gen.TENSOR_V) for f in range(N)], "bf16")
+    if wl.recipe == "stress":
+        wdev.fill_stress_keys(k.view(N, Hkv, T, d), wl, 0, range(N))
+    else:
+        wdev.fill_iid(k, [gen.stream_key(wl.seed, 0, f, gen.TENSOR_K) for f in range(N)], "bf16")
+    out = torch.empty((1, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    st = FrameStepper.from_workload(wl, stream=stream)
+    heater = Heater(wl, q, k, v, out, stream)
+    try:
+        for f in range(N):
+            st.step(q[f], k[f], v[f], out)
+        ms, secs = timed_videos(st, heater, q, k, v, out, n_videos, heat_frames)
+    finally:
+        heater.close()
+        st.close()
+    del q, k, v
+    full = wl.full_from_frame
+    att = ms[:, full:, 0]
+    alg = attention_flops(wl, wl.capacity)
+    exe = executed_mfma_flops(wl, wl.capacity)
+    tf = alg / (att.mean() * 1e-3) / 1e12
+    res = {"workload": name, "layers": 1, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "tokens_per_frame": T,
+           "frames_per_video": N, "capacity": wl.capacity,
+           "inputs": "i.i.d. N(0,1) bf16" + (", keys with heavy rows and exact duplicates" if wl.recipe == "stress"
+                                            else ""),
+           "videos": n_videos, "frames_per_s": round(float(np.median(N / secs)), 2),
+           "frames_per_s_events": round(float(np.median(N / (ms.sum(axis=2).sum(axis=1) * 1e-3))), 2),
+           "attention_ms_state_full": round(float(att.mean()), 4),
+           "refresh_ms_state_full": round(float(ms[:, full:, 1].mean()), 4),
+           "attention_tflops": round(tf, 1), "attention_frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+           "executed_mfma_frac": round(exe / (att.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+    res.update(curve_summary(ms.sum(axis=2), full, every=max(1, N // 32)))
+    print(f"[bench] {name}: {res['frames_per_s']} frames/s over whole videos", file=sys.stderr, flush=True)
+    return res
+
+
+def refresh_stages(wl, q_all, k_all, v_all, out, stream, timed=64):
+    """The refresh as three launches (context option split_refresh): selection, state update
+    and decode-cache append timed one by one with HIP events at state full, each stage's
+    algorithmic bytes over its time, against the 8 TB/s HBM peak."""
+    from paper_2605_31598_amd import FrameStepper
+    import torch
+
+    full, T, L = wl.full_from_frame, wl.tokens_per_frame, wl.n_layers
+    st = FrameStepper.from_workload(wl, stream=stream, split_refresh=True)
+    admitted = []
+    try:
+        for f in range(full + 8):
+            st.step(q_all[f], k_all[f], v_all[f], out)
+        torch.cuda.synchronize()
+        st.timing_start(timed)
+        for f in range(full + 8, full + 8 + timed):
+            st.step(q_all[f], k_all[f], v_all[f], out)
+        ms = st.timing_stop(timed).astype(np.float64)
+        last_pos0 = wl.pos_offset + (full + 8 + timed - 1) * T
+        admitted = float(np.mean([(st.read_state(l)["pos"] >= last_pos0).sum(axis=1).mean() for l in range(L)]))
+    finally:
+        st.close()
+    n_qtiles = -(-(wl.group * T) // 256)
+    b = refresh_stage_bytes(wl, wl.capacity, n_qtiles, admitted)
+    res = {"kernels": {"select": "refresh_kernel (selection launch)", "update": "refresh_update_kernel",
+                       "append": "refresh_append_kernel"},
+           "timed_frames_at_state_full": timed, "admitted_rows_per_head": round(admitted, 1)}
+    for i, key in ((1, "select"), (2, "update"), (3, "append")):
+        t = float(ms[:, i].mean())
+        gbs = b[key] / (t * 1e-3) / 1e9
+        res[key] = {"ms": round(t, 4), "bytes": float(b[key]), "GBps": round(gbs, 1),
+                    "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
+    res["three_launches_ms"] = round(float(ms[:, 1:].sum(axis=1).mean()), 4)
+    return res
+
+
+def oracle_timings(budget_s=20.0):
+    """The oracle timing plan beside the headline cpu_baseline: the tiny fp32 layer (whole
+    video) and the 7B-shaped single layer from state-full on, with all BLAS threads and with
+    one, each on a bounded number of layer-frames."""
+    from oracle import statekv_oracle as orc
+    from workloads import CONFIGS
+    from workloads import generate as gen
+
+    def run(wl, frames, state):
+        times = []
+        for n in frames:
+            x = gen.frame_inputs_f64(wl, 0, n)
+            t0 = time.perf_counter()
+            r = orc.frame_step(state, x["q"], x["k"], x["v"], n, wl.capacity, wl.scale, wl.pos_offset)
+            times.append(time.perf_counter() - t0)
+            state = r.state
+        return times, state
+
+    res = {}
+    c1 = CONFIGS["tiny_f32"]
+    t, _ = run(c1, range(c1.n_frames), orc.LayerState.empty(c1.n_kv_heads, c1.head_dim))
+    res["tiny_f32"] = {"layer_frames": len(t), "ms_per_layer_frame": round(1e3 * float(np.mean(t)), 3),
+                       "frames_per_s": round(1.0 / float(np.mean(t)), 1)}
+    c2 = CONFIGS["vlm7b_1layer"]
+    _, state = run(c2, range(c2.full_from_frame), orc.LayerState.empty(c2.n_kv_heads, c2.head_dim))
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threadpool_limits, threads = None, len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    n_max = c2.n_frames - c2.full_from_frame
+    times, st2 = [], state
+    n = c2.full_from_frame
+    while n < c2.n_frames and time.perf_counter() - t0 < budget_s / 2:
+        t, st2 = run(c2, [n], st2)
+        times += t
+        n += 1
+    res["vlm7b_1layer"] = {"threads": int(threads), "layer_frames": len(times),
+                           "ms_per_layer_frame": round(1e3 * float(np.mean(times)), 2)}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            times1, st1, n = [], state, c2.full_from_frame
+            while n < c2.full_from_frame + n_max and time.perf_counter() - t0 < budget_s / 2:
+                t, st1 = run(c2, [n], st1)
+                times1 += t
+                n += 1
+        res["vlm7b_1layer_1_thread"] = {"threads": 1, "layer_frames": len(times1),
+                                        "ms_per_layer_frame": round(1e3 * float(np.mean(times1)), 2)}
+    res["host_cores"] = len(os.sched_getaffinity(0))
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1536, help="timed frames (the video restarts after its last frame)")
-    ap.add_argument("--warmup", type=int, default=512, help="untimed frames before timing")
+    ap.add_argument("--steps", type=int, default=1536, help="timed frames, all at state full")
+    ap.add_argument("--warmup", type=int, default=512, help="untimed state-full frames before timing")
     ap.add_argument("--workload", default="vlm7b_28layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-baselines", action="store_true",
-                    help="skip the runs reported beside the main line (Full SA, recency window, YaRN, decode, "
-                         "diagnostics, the 72B-shaped stack)")
+                    help="skip the runs reported beside the main line (whole-video curves, one-layer lines, refresh "
+                         "stages, Full SA, recency window, YaRN, decode, diagnostics, the 72B-shaped stack)")
+    ap.add_argument("--split-refresh", action="store_true",
+                    help="time the main line with the refresh as three launches (for per-stage counters)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -437,53 +697,60 @@ def main():
     print(f"[bench] {wl.name}: inputs resident ({(q_all.numel() + k_all.numel() + v_all.numel()) * 2 / 1e9:.1f} GB)",
           file=sys.stderr, flush=True)
 
-    st = FrameStepper.from_workload(wl, stream=stream)
-    counter = {"i": 0}
-
-    def run(n_frames):
-        for _ in range(n_frames):
-            f = counter["i"] % N
-            if f == 0 and counter["i"] > 0:
-                st.reset()
+    # Video streams filled to state-full (frames 0 .. full-1, untimed); the warm-up and
+    # timed steps walk through their state-full frames, one stream after another.
+    full = wl.full_from_frame
+    per_stream = N - full
+    n_streams = -(-(args.warmup + args.steps) // per_stream)
+    streams = [FrameStepper.from_workload(wl, stream=stream, split_refresh=args.split_refresh)
+               for _ in range(n_streams)]
+    for st in streams:
+        for f in range(full):
             st.step(q_all[f], k_all[f], v_all[f], out)
-            counter["i"] += 1
+    slots = [(i, f) for i in range(n_streams) for f in range(full, N)]
 
-    run(args.warmup)
-    torch.cuda.synchronize()
-    first_frame = counter["i"] % N
-    st.timing_start(args.steps)
+    def run(lo, hi):
+        for i, f in slots[lo:hi]:
+            streams[i].step(q_all[f], k_all[f], v_all[f], out)
+
+    # events for the warm-up and timed steps of every stream are created first (the host
+    # takes a while, the device idles), so the warm-up steps run right before the timed ones
+    recorded = slots[:args.warmup + args.steps]
+    used = sorted({i for i, _ in recorded})
+    for i in used:
+        streams[i].timing_start(sum(1 for j, _ in recorded if j == i))
+    run(0, args.warmup)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run(args.steps)
+    run(args.warmup, args.warmup + args.steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    stages = st.timing_stop(args.steps)  # [K, 2] ms: attention, refresh
+    timed = slots[args.warmup:args.warmup + args.steps]
+    stages = np.concatenate([streams[i].timing_stop(args.warmup + args.steps) for i in used]).astype(np.float64)
+    stages = stages[args.warmup:]  # [K, stages] of the timed steps
     # rows admitted by the last timed frame (its positions are the newest in the state)
-    last_pos0 = wl.pos_offset + ((counter["i"] - 1) % N) * T
-    admitted = float(np.mean([(st.read_state(l)["pos"] >= last_pos0).sum(axis=1).mean() for l in range(L)]))
-    st.close()
+    i_last, f_last = timed[-1]
+    last_pos0 = wl.pos_offset + f_last * T
+    admitted = float(np.mean([(streams[i_last].read_state(l)["pos"] >= last_pos0).sum(axis=1).mean()
+                              for l in range(L)]))
+    for st in streams:
+        st.close()
+    del streams
     elapsed = t1 - t0
     fps = args.steps / elapsed
-    print(f"[bench] timed {args.steps} frames in {elapsed:.3f} s", file=sys.stderr, flush=True)
+    print(f"[bench] timed {args.steps} state-full frames in {elapsed:.3f} s", file=sys.stderr, flush=True)
 
-    frames = (first_frame + np.arange(args.steps)) % N
-    S = np.minimum(wl.capacity, frames * T)
-    attn_ms = stages[:, 0].astype(np.float64)
-    alg = np.array([attention_flops(wl, int(s)) for s in S], dtype=np.float64)
-    exe = np.array([executed_mfma_flops(wl, int(s)) for s in S], dtype=np.float64)
-    achieved = alg.sum() / (attn_ms.sum() * 1e-3) / 1e12
-    executed = exe.sum() / (attn_ms.sum() * 1e-3) / 1e12
+    S = wl.capacity
+    attn_ms = stages[:, 0]
+    alg = attention_flops(wl, S)
+    exe = executed_mfma_flops(wl, S)
+    achieved = alg / (attn_ms.mean() * 1e-3) / 1e12
+    executed = exe / (attn_ms.mean() * 1e-3) / 1e12
     n_qtiles = -(-(wl.group * T) // 256)
-    ref_b = np.array([refresh_bytes(wl, int(s), n_qtiles, admitted) for s in S], dtype=np.float64)
-    refresh_gbs = float(ref_b.sum() / (stages[:, 1].astype(np.float64).sum() * 1e-3) / 1e9)
-
+    ref_b = refresh_bytes(wl, S, n_qtiles, admitted)
+    refresh_ms = stages[:, 1:].sum(axis=1)
+    refresh_gbs = float(ref_b / (refresh_ms.mean() * 1e-3) / 1e9)
     frame_ms = stages.sum(axis=1)
-    full = frames >= wl.full_from_frame
-    per_index = {}
-    for f, ms in zip(frames[full], frame_ms[full]):
-        per_index.setdefault(int(f), []).append(float(ms))
-    med_by_frame = np.array([np.median(v) for _, v in sorted(per_index.items())]) if per_index else np.array([0.0])
-    med = float(np.median(med_by_frame))
     traffic = stored_traffic()
 
     result = {
@@ -501,7 +768,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "tokens_per_frame": T, "frames_per_video": N, "capacity": wl.capacity,
-                   "layers_per_call": L, "inputs": "i.i.d. N(0,1) bf16, generated in HBM"},
+                   "layers_per_call": L, "timed_frames": f"state-full frames {full}..{N - 1} of 512-frame videos",
+                   "refresh_launches": 3 if args.split_refresh else 1,
+                   "inputs": "i.i.d. N(0,1) bf16, generated in HBM"},
         "roofline": {
             "bound": "mfma",
             "achieved": round(achieved, 2),
@@ -510,31 +779,37 @@ def main():
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
             "kernel": "attn_mfma_kernel<128>",
-            "flops_per_launch": float(alg.mean()),
+            "flops_per_launch": float(alg),
             "avg_launch_ms": float(attn_ms.mean()),
             "executed_mfma_tflops": round(executed, 2),
             "executed_frac": round(executed / PEAK_BF16_TFLOPS, 4),
         },
-        "stages_ms_mean": {n: float(stages[:, i].mean()) for i, n in enumerate(("attention", "refresh"))},
+        "stages_ms_mean": {"attention": float(attn_ms.mean()), "refresh": float(refresh_ms.mean())},
         "hbm": {
             "kernel": "refresh_kernel (selection + state update + decode-cache append)",
-            "bytes_per_launch": float(ref_b.mean()),
+            "bytes_per_launch": float(ref_b),
             "admitted_rows_per_head": round(admitted, 1),
             "GBps": round(refresh_gbs, 1),
             "peak_GBps": PEAK_HBM_GBS,
             "frac": round(refresh_gbs / PEAK_HBM_GBS, 4),
         },
         "latency": {
-            "frame_ms_median_state_full": round(med, 4),
-            "flatness_max_dev": round(float(np.max(np.abs(med_by_frame / med - 1.0))), 4) if med > 0 else None,
-            "frame_ms_first_frames": [round(float(x), 4) for x in frame_ms[:min(16, len(frame_ms))]],
-            "from_frame": int(wl.full_from_frame),
+            "frame_ms_median": round(float(np.median(frame_ms)), 4),
+            "frame_ms_p10_p90": [round(float(np.percentile(frame_ms, 10)), 4),
+                                 round(float(np.percentile(frame_ms, 90)), 4)],
         },
     }
     if not args.no_baselines:
-        result["baselines"] = baselines(wl, q_all, k_all, v_all, out, stream, med)
+        result["video"] = video_curve(wl, q_all, k_all, v_all, out, stream)
+        result["hbm"]["stages"] = refresh_stages(wl, q_all, k_all, v_all, out, stream)
+        result["baselines"] = baselines(wl, q_all, k_all, v_all, out, stream,
+                                        result["video"]["frame_ms_median_state_full"])
         result["decode"] = decode_bench(wl, q_all, k_all, v_all, out, stream)
         result["per_layer"] = per_layer_bench(wl, q_all, k_all, v_all, out, stream)
+        del q_all, k_all, v_all
+        torch.cuda.empty_cache()
+        result["vlm7b_1layer"] = single_layer_line("vlm7b_1layer", stream, heat_frames=768)
+        result["stress_1layer"] = single_layer_line("stress_1layer", stream, heat_frames=128)
         result["diagnostics"] = diagnostics_bench(stream)
         result["vlm72b"] = large_bench(stream)
         result["vlm72b_shard8"] = large_bench(stream, kv_heads=1)
@@ -542,6 +817,8 @@ def main():
         result["hbm"]["frac_of_copy"] = round(result["hbm"]["GBps"] / result["hbm"]["copy_GBps"], 4)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        if not args.no_baselines:
+            result["oracle_timings"] = oracle_timings()
     print(json.dumps(result), flush=True)
 
 

@@ -420,14 +420,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     else
       sweep1(std::integral_constant<int, kKT / 32>{});
 
-    // the other 16 keys of every 32-key block live in lane ^ 32
+    // The other 16 keys of every 32-key block live in lane ^ 32.  Both lanes merge
+    // in one operand order (h = 0's statistics first; the merge rounds differently
+    // with the operands swapped), so the two lanes of a row hold bit-identical
+    // statistics and equal keys get equal column sums wherever they sit in a block.
     const float mo = __shfl_xor(m, 32, 64);
     const float lo = __shfl_xor(l, 32, 64);
-    float mm = fmaxf(m, mo);
-    float ll = l * fast_exp2((m - mm) * c) + lo * fast_exp2((mo - mm) * c);
+    const float ma = h ? mo : m, la = h ? lo : l, mb = h ? m : mo, lb = h ? l : lo;
+    float mm = fmaxf(ma, mb);
+    float ll = la * fast_exp2((ma - mm) * c) + lb * fast_exp2((mb - mm) * c);
     if (split) {
       // the other key half of these rows is wave ^ 4's; exchanged through the
-      // second column-sum buffer, first written after sweep 2's first barrier
+      // second column-sum buffer, first written after sweep 2's first barrier;
+      // merged with the first half's statistics first in both waves
       float* xm = &sm.cs[1][wave][0];
       if (h == 0) {
         xm[l32] = mm;
@@ -436,8 +441,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
       __syncthreads();
       const float* pm = &sm.cs[1][wave ^ 4][0];
       const float mp = pm[l32], lp = pm[32 + l32];
-      const float mt = fmaxf(mm, mp);
-      ll = ll * fast_exp2((mm - mt) * c) + lp * fast_exp2((mp - mt) * c);
+      const float m0 = grp ? mp : mm, l0 = grp ? lp : ll, m1 = grp ? mm : mp, l1 = grp ? ll : lp;
+      const float mt = fmaxf(m0, m1);
+      ll = l0 * fast_exp2((m0 - mt) * c) + l1 * fast_exp2((m1 - mt) * c);
       mm = mt;
     }
     if (a.mode == 1) {

@@ -83,6 +83,9 @@ def test_stress_stream_past_state_full():
     s = run_tracking(wl, n, [0], log_every=8)
     say(f"stress_1layer frames 0..{n - 1}: {s}")
     _assert_divergences_at_near_ties(s)
+    # exact ties of the oracle (duplicate keys) are exact on the GPU too, and go the same way
+    assert all(d["gap"] > 0.0 for d in s["divergences"]), s["divergences"]
+    assert s["straddle_gpu"] == s["straddle_oracle"] > 0
 
 
 # --------------------------------------------------------------------------
