@@ -143,6 +143,21 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
 skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count,
                           const void* q, const void* k, const void* v, void* out);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): skv_frame_step with the
+ * same arguments, layouts, results (bit for bit) and errors, except that the
+ * per-call scratch of the step (column-sum partials, key-split row statistics and
+ * output shares, admit lists) lives in one static device array of the library,
+ * 64 MiB per device, instead of the context's buffers.  The call allocates and
+ * frees nothing and calls no allocating routine.  A call needing more than 64 MiB
+ * of scratch returns SKV_ERR_UNSUPPORTED with nothing enqueued (e.g. all 80 layers
+ * of the 72B-shaped stack in one call; one layer per call fits).  Every call on a
+ * device shares that device's array and leaves it holding its own partial
+ * results; nothing in it has to start at zero.  Calls that overlap on one device
+ * (contexts on different streams) race on the array: serialise them. */
+skv_status skv_frame_step_noalloc(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count,
+                                  const void* q, const void* k, const void* v, void* out);
+
 /* Decoding after (or between) frames reads the detailed state D, not C (the
  * decoding paragraph of the method).  Runs layers [layer_begin, layer_begin +
  * layer_count) for n_tokens new tokens: each attends to every video token of

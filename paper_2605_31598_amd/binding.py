@@ -39,7 +39,8 @@ STAGES = ("attention", "refresh", "state_update", "append")
 
 # Every symbol declared in include/statekv.h.
 EXPORTS = (
-    "skv_init", "skv_frame_step", "skv_decode_step", "skv_state_view", "skv_decode_cache_view", "skv_reset", "skv_seek",
+    "skv_init", "skv_frame_step", "skv_frame_step_noalloc", "skv_decode_step", "skv_state_view",
+    "skv_decode_cache_view", "skv_reset", "skv_seek",
     "skv_timing_start", "skv_timing_stop", "skv_destroy", "skv_status_string", "skv_last_error",
 )
 
@@ -95,6 +96,8 @@ def load_library(path: str = LIB_PATH):
     lib.skv_init.argtypes = [P(skv_config), ctypes.c_void_p, P(ctypes.c_void_p)]
     lib.skv_frame_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.skv_frame_step_noalloc.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.skv_decode_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.skv_state_view.argtypes = [ctypes.c_void_p, ctypes.c_int32, P(skv_state_view_t)]
@@ -109,7 +112,8 @@ def load_library(path: str = LIB_PATH):
     lib.skv_status_string.restype = ctypes.c_char_p
     lib.skv_last_error.argtypes = []
     lib.skv_last_error.restype = ctypes.c_char_p
-    for name in ("skv_init", "skv_frame_step", "skv_state_view", "skv_decode_cache_view", "skv_reset",
+    for name in ("skv_init", "skv_frame_step", "skv_frame_step_noalloc", "skv_decode_step", "skv_state_view",
+                 "skv_decode_cache_view", "skv_reset",
                  "skv_seek", "skv_timing_start", "skv_timing_stop"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -149,6 +153,12 @@ def skv_frame_step(ctx: int, layer_begin: int, layer_count: int, q: int, k: int,
     _check(load_library().skv_frame_step(ctypes.c_void_p(ctx), layer_begin, layer_count, ctypes.c_void_p(q),
                                          ctypes.c_void_p(k), ctypes.c_void_p(v), ctypes.c_void_p(out)),
            "skv_frame_step")
+
+
+def skv_frame_step_noalloc(ctx: int, layer_begin: int, layer_count: int, q: int, k: int, v: int, out: int) -> None:
+    _check(load_library().skv_frame_step_noalloc(ctypes.c_void_p(ctx), layer_begin, layer_count, ctypes.c_void_p(q),
+                                                 ctypes.c_void_p(k), ctypes.c_void_p(v), ctypes.c_void_p(out)),
+           "skv_frame_step_noalloc")
 
 
 def skv_decode_step(ctx: int, layer_begin: int, layer_count: int, n_tokens: int, q: int, k: int, v: int,

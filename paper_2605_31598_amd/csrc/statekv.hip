@@ -18,6 +18,7 @@
 #include <cstdlib>
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -91,6 +92,7 @@ struct skv_ctx {
   std::vector<Plan> plans;
   float* split_stats = nullptr;    // key-split plans: per-range row statistics and output shares,
   float* split_out = nullptr;      // sized for the largest such plan (null if none)
+  void* scratch = nullptr;         // this device's static scratch (skv_frame_step_noalloc)
   std::vector<void*> allocations;
 
   // progress of the stream
@@ -242,6 +244,43 @@ skv_status build_plans(skv_ctx* c, int rows) {
   return SKV_OK;
 }
 
+// Scratch of skv_frame_step_noalloc: the per-call buffers of a frame step (column-sum
+// partials, key-split row statistics and output shares, admit lists) in one static
+// device array, so that the call allocates nothing.  Each device the library runs
+// on holds its own copy until the process ends.  In host code `scratch` only names
+// the symbol: its device address on the current device comes from
+// hipGetSymbolAddress, taken once per device at skv_init and used from then on.
+constexpr size_t kScratchBytes = size_t{64} << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of `scratch` on `device` (current), resolved on first use.
+hipError_t scratch_address(int device, void** out) {
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_addr[device] == nullptr) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[device] = ptr;
+  }
+  *out = g_scratch_addr[device];
+  return hipSuccess;
+}
+
+// Per-call buffers of a frame step.
+struct StepScratch {
+  float* partial;       // [layer_count * H_kv][tile_stride][pool_stride]
+  float* split_stats;   // [layer_count * H_kv][n_ks][G * T][2]
+  float* split_out;     // [n_ks][layer_count][H_q][T][d]
+  int32_t* admit_src;   // [layer_count * H_kv][T]
+  int32_t* admit_dst;
+  int32_t* admit_count; // [layer_count * H_kv]
+};
+
 }  // namespace
 
 extern "C" {
@@ -322,6 +361,11 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
     delete ctx;
     return hip_fail(e, "hipGetDevice");
   }
+  e = scratch_address(ctx->device, &ctx->scratch);
+  if (e != hipSuccess) {
+    delete ctx;
+    return hip_fail(e, "hipGetSymbolAddress of the static scratch");
+  }
   e = skv::prepare_kernels(c.head_dim, c.dtype == SKV_BF16, ctx->pool_stride);
   if (e != hipSuccess) {
     delete ctx;
@@ -378,8 +422,13 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   return SKV_OK;
 }
 
-skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, const void* q, const void* k,
-                          const void* v, void* out) {
+}  // extern "C"
+
+namespace {
+
+// Argument, order and capacity checks of a frame step (nothing enqueued).
+skv_status check_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, const void* q, const void* k,
+                            const void* v, void* out) {
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
   if (q == nullptr || k == nullptr || v == nullptr || out == nullptr)
     return fail(SKV_ERR_INVALID_ARG, "q, k, v and out must be device pointers");
@@ -393,7 +442,45 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
     return fail(SKV_ERR_ORDER, "expected layer_begin = " + std::to_string(ctx->next_layer));
   if (ctx->dec_next_layer != 0) return fail(SKV_ERR_ORDER, "a decode call is half done");
   if (ctx->frame >= c.max_frames) return fail(SKV_ERR_CAPACITY, "decode cache is full (max_frames reached)");
+  return SKV_OK;
+}
 
+// Scratch bytes a frame step of layer_count layers needs (each buffer 256-byte aligned),
+// and the buffers carved from `base` when base is not null.
+size_t carve_scratch(const skv_ctx* ctx, int32_t layer_count, char* base, StepScratch* sc) {
+  const skv_config& c = ctx->cfg;
+  const size_t LH = static_cast<size_t>(layer_count) * c.n_kv_heads;
+  const size_t rows = static_cast<size_t>(ctx->G) * c.tokens_per_frame;
+  const size_t n_ks = static_cast<size_t>(ctx->plans[static_cast<size_t>(layer_count - 1)].n_ks);
+  const bool full = c.policy == SKV_POLICY_FULL;
+  const size_t sizes[6] = {
+      full ? 0 : LH * ctx->tile_stride * ctx->pool_stride * sizeof(float),
+      n_ks > 1 ? LH * n_ks * rows * 2 * sizeof(float) : 0,
+      n_ks > 1 ? n_ks * layer_count * c.n_q_heads * c.tokens_per_frame * c.head_dim * sizeof(float) : 0,
+      LH * c.tokens_per_frame * sizeof(int32_t),
+      LH * c.tokens_per_frame * sizeof(int32_t),
+      LH * sizeof(int32_t)};
+  void* ptrs[6];
+  size_t off = 0;
+  for (int i = 0; i < 6; ++i) {
+    ptrs[i] = sizes[i] > 0 && base != nullptr ? base + off : nullptr;
+    off += (sizes[i] + 255) / 256 * 256;
+  }
+  if (sc != nullptr) {
+    sc->partial = static_cast<float*>(ptrs[0]);
+    sc->split_stats = static_cast<float*>(ptrs[1]);
+    sc->split_out = static_cast<float*>(ptrs[2]);
+    sc->admit_src = static_cast<int32_t*>(ptrs[3]);
+    sc->admit_dst = static_cast<int32_t*>(ptrs[4]);
+    sc->admit_count = static_cast<int32_t*>(ptrs[5]);
+  }
+  return off;
+}
+
+// The launch sequence of a checked frame step, with the per-call buffers in `sc`.
+skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, const void* q, const void* k,
+                              const void* v, void* out, const StepScratch& sc) {
+  const skv_config& c = ctx->cfg;
   const int T = c.tokens_per_frame, Hkv = c.n_kv_heads, B = c.capacity, d = c.head_dim;
   const int S = state_size(ctx, ctx->frame);
   const int32_t pos0 = static_cast<int32_t>(c.pos_offset + ctx->frame * T);
@@ -431,7 +518,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   }
   aa.out = out;
   const skv_ctx::Plan& plan = ctx->plans[static_cast<size_t>(layer_count - 1)];
-  aa.partial = full ? nullptr : ctx->partial + lh0 * ctx->tile_stride * ctx->pool_stride;
+  aa.partial = full ? nullptr : sc.partial;
   aa.work = plan.work;
   aa.n_work = plan.n_work;
   aa.rope_tab = ctx->rope_tab;
@@ -448,8 +535,8 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   aa.scale_log2 = ctx->scale_log2;
   aa.mode = 0;
   aa.n_ks = plan.n_ks;
-  aa.stats = ctx->split_stats;
-  aa.opart = ctx->split_out;
+  aa.stats = sc.split_stats;
+  aa.opart = sc.split_out;
 
   skv::RefreshArgs ra;
   ra.partial = aa.partial;
@@ -467,9 +554,9 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.state_score = ctx->state_score + lh0 * B;
   ra.pool_score = ctx->pool_score + lh0 * ctx->pool_stride;
   ra.pool_pos = ctx->pool_pos + lh0 * ctx->pool_stride;
-  ra.admit_src = ctx->admit_src + lh0 * T;
-  ra.admit_dst = ctx->admit_dst + lh0 * T;
-  ra.admit_count = ctx->admit_count + lh0;
+  ra.admit_src = sc.admit_src;
+  ra.admit_dst = sc.admit_dst;
+  ra.admit_count = sc.admit_count;
   ra.split_update = false;
   ra.ck = static_cast<char*>(ctx->cache_k) + lh0 * ctx->max_tokens * rb;
   ra.cv = static_cast<char*>(ctx->cache_v) + lh0 * ctx->max_tokens * rb;
@@ -486,7 +573,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   ra.mode = c.policy == SKV_POLICY_RECENT ? 1 : 0;
   // key-split plans: the refresh launch also adds the attention's output shares
   ra.n_ks = ctx->use_mfma && !full ? plan.n_ks : 1;
-  ra.opart = ctx->split_out;
+  ra.opart = sc.split_out;
   ra.out = out;
   ra.out_elems = static_cast<int64_t>(layer_count) * c.n_q_heads * T * d;
   ra.n_comb = static_cast<int>(std::min<int64_t>(128, (ra.out_elems / 4 + skv::kSelectThreads - 1) / skv::kSelectThreads));
@@ -537,6 +624,40 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
     ++ctx->frame;
   }
   return SKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, const void* q, const void* k,
+                          const void* v, void* out) {
+  const skv_status s = check_frame_step(ctx, layer_begin, layer_count, q, k, v, out);
+  if (s != SKV_OK) return s;
+  const skv_config& c = ctx->cfg;
+  const size_t lh0 = static_cast<size_t>(layer_begin) * c.n_kv_heads;
+  StepScratch sc;
+  sc.partial = ctx->partial != nullptr ? ctx->partial + lh0 * ctx->tile_stride * ctx->pool_stride : nullptr;
+  sc.split_stats = ctx->split_stats;
+  sc.split_out = ctx->split_out;
+  sc.admit_src = ctx->admit_src + lh0 * c.tokens_per_frame;
+  sc.admit_dst = ctx->admit_dst + lh0 * c.tokens_per_frame;
+  sc.admit_count = ctx->admit_count + lh0;
+  return enqueue_frame_step(ctx, layer_begin, layer_count, q, k, v, out, sc);
+}
+
+skv_status skv_frame_step_noalloc(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, const void* q,
+                                  const void* k, const void* v, void* out) {
+  const skv_status s = check_frame_step(ctx, layer_begin, layer_count, q, k, v, out);
+  if (s != SKV_OK) return s;
+  const size_t need = carve_scratch(ctx, layer_count, nullptr, nullptr);
+  if (need > kScratchBytes)
+    return fail(SKV_ERR_UNSUPPORTED, "this call needs " + std::to_string(need) + " bytes of scratch, the static " +
+                                         "scratch holds " + std::to_string(kScratchBytes) +
+                                         "; step fewer layers per call or use skv_frame_step");
+  StepScratch sc;
+  carve_scratch(ctx, layer_count, static_cast<char*>(ctx->scratch), &sc);
+  return enqueue_frame_step(ctx, layer_begin, layer_count, q, k, v, out, sc);
 }
 
 skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count, int32_t n_tokens,
