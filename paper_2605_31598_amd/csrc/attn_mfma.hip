@@ -33,8 +33,9 @@
 //     probabilities are known only after the row statistics, and recomputing
 //     K Q^T is cheaper than storing the logits.
 //   * Tiles that contain frame keys (the only ones with masked entries) run in a
-//     separate loop, keeping mask code off the common path; tiles wholly inside
-//     the state are copied with per-lane offsets fixed once per launch.
+//     separate loop, keeping mask code off the common path; there a wave skips the
+//     32-key blocks that lie wholly past the causal limit of all its rows.  Tiles
+//     wholly inside the state are copied with per-lane offsets fixed once per launch.
 //   * The host plan keeps the row tiles of one (layer, KV head) on one XCD so
 //     they share K/V in that XCD's L2.
 //
@@ -130,10 +131,11 @@ __device__ inline void lgkm_wait(T& x) {
 //   key(lane) = 8 * (b3 + 2 * b4) + 4 * h + (b1 + 2 * b2)     (bN = bit N of lane)
 // within the 32-key block; lanes differing only in bit 0 return the same key.
 // Reduce-scatter: each step halves the values a lane carries while pairing
-// lanes that differ in one more row bit.  The first step pairs lanes l and
-// l ^ 16 and applies the weights: w0 and w1 are the weights of the first and the
-// second value the swap leaves in this lane (own and partner row for b4 = 0,
-// partner and own row for b4 = 1).
+// lanes that differ in one more row bit (partners l ^ 16, l ^ 8, l ^ 4, l ^ 3,
+// l ^ 1: the same pairing of rows for every key, so equal columns give equal
+// sums).  The first step applies the weights: w0 and w1 are the weights of the
+// first and the second value the swap leaves in this lane (own and partner row for
+// b4 = 0, partner and own row for b4 = 1).
 __device__ inline float column_reduce(const float (&e)[16], int lane, float w0, float w1) {
   float c1[8];
 #pragma unroll
@@ -142,21 +144,30 @@ __device__ inline float column_reduce(const float (&e)[16], int lane, float w0, 
                                                      false, false);
     c1[v] = fmaf(__uint_as_float(pr[0]), w0, __uint_as_float(pr[1]) * w1);
   }
-  const bool b3 = lane & 8, b2 = lane & 4, b1 = lane & 2;
-  float c2[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {  // lanes i <-> i^8 inside a row
-    const float keep = b3 ? c1[v + 4] : c1[v];
-    const float send = b3 ? c1[v] : c1[v + 4];
-    c2[v] = keep + dpp_f<0x128>(send);
-  }
-  float c3[2];
-#pragma unroll
-  for (int v = 0; v < 2; ++v) {  // lanes i <-> 7-i inside each half row (bit 2 differs)
-    const float keep = b2 ? c2[v + 2] : c2[v];
-    const float send = b2 ? c2[v] : c2[v + 2];
-    c3[v] = keep + dpp_f<0x141>(send);
-  }
+  // Lanes i <-> i ^ 8, then i <-> i ^ 4, inside each row of 16 lanes.  A lane keeps
+  // one of its two values by bit 3 (then bit 2) of its index, and the bank masks of
+  // the DPP adds pick the lanes: lanes 0-7 of a row (banks 0, 1) add their partner's
+  // first value to their own, lanes 8-15 (banks 2, 3) the second; then banks 0, 2
+  // (bit 2 clear) and 1, 3 (bit 2 set).  Two adds per pair, no selects.  The leading
+  // s_nop covers the VALU-write to DPP-read hazard on c1; inside the block every
+  // DPP source was written at least two instructions earlier.
+  const bool b1 = lane & 2;
+  float c2[4], c3[2];
+  asm("s_nop 1\n"
+      "v_add_f32_dpp %0, %6, %6 row_ror:8 row_mask:0xf bank_mask:0x3\n"
+      "v_add_f32_dpp %1, %7, %7 row_ror:8 row_mask:0xf bank_mask:0x3\n"
+      "v_add_f32_dpp %2, %8, %8 row_ror:8 row_mask:0xf bank_mask:0x3\n"
+      "v_add_f32_dpp %3, %9, %9 row_ror:8 row_mask:0xf bank_mask:0x3\n"
+      "v_add_f32_dpp %0, %10, %10 row_ror:8 row_mask:0xf bank_mask:0xc\n"
+      "v_add_f32_dpp %1, %11, %11 row_ror:8 row_mask:0xf bank_mask:0xc\n"
+      "v_add_f32_dpp %2, %12, %12 row_ror:8 row_mask:0xf bank_mask:0xc\n"
+      "v_add_f32_dpp %3, %13, %13 row_ror:8 row_mask:0xf bank_mask:0xc\n"
+      "v_add_f32_dpp %4, %0, %0 row_shl:4 row_mask:0xf bank_mask:0x5\n"
+      "v_add_f32_dpp %5, %1, %1 row_shl:4 row_mask:0xf bank_mask:0x5\n"
+      "v_add_f32_dpp %4, %2, %2 row_shr:4 row_mask:0xf bank_mask:0xa\n"
+      "v_add_f32_dpp %5, %3, %3 row_shr:4 row_mask:0xf bank_mask:0xa"
+      : "=&v"(c2[0]), "=&v"(c2[1]), "=&v"(c2[2]), "=&v"(c2[3]), "=&v"(c3[0]), "=&v"(c3[1])
+      : "v"(c1[0]), "v"(c1[1]), "v"(c1[2]), "v"(c1[3]), "v"(c1[4]), "v"(c1[5]), "v"(c1[6]), "v"(c1[7]));
   const float keep = b1 ? c3[1] : c3[0];  // lanes i <-> 3-i inside a quad (bit 1 differs)
   const float send = b1 ? c3[0] : c3[1];
   const float c4 = keep + dpp_f<0x1B>(send);
@@ -216,6 +227,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const int r_lane = row0 + l32;
   const bool row_valid = r_lane < row_end;
   const int lim = row_valid ? S + (r_lane % a.T) : -1;  // candidate j is visible iff j <= lim
+  // The wave's largest limit (a scalar): in tiles with frame keys, the 32-key blocks
+  // past it are masked for every row of the wave and are skipped.
+  int wlim = lim;
+#pragma unroll
+  for (int off = 16; off > 0; off >>= 1) wlim = max(wlim, __shfl_xor(wlim, off, 64));
+  wlim = __builtin_amdgcn_readfirstlane(wlim);
   bf16x8 qreg[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
@@ -340,9 +357,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     u32x4 kop[KS];
     if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
     if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, false, pure_next);
+    // masked tiles: blocks whose first key is past the wave's limit (a suffix) are skipped
+    const int first = t * kKT + key0;
+    const int na = !decltype(masked)::value ? NB : wlim < first ? 0 : min(NB, (wlim - first) / 32 + 1);
     if (active) {
       static_for<NB>([&](auto kbc) {
         constexpr int KB = decltype(kbc)::value;
+        if constexpr (decltype(masked)::value) {
+          if (KB >= na) return;
+        }
         const f32x16 acc = qk_mfma(kop);
         if constexpr (KB + 1 < NB) issue_k(std::integral_constant<int, KB + 1>{}, kaddr, kop);
         f32x16 accv = acc;
@@ -472,7 +495,85 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const int tr_row = 4 * h + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  auto sweep2_tile = [&](int t, auto masked, auto pure_next, auto nbc) {
+  // End of a sweep-2 tile: wait for the next tile's copies, then the cross-wave
+  // column sums of tile t -> this row tile's partials; buffer b is written again
+  // only after the next barrier.  In a split workgroup a key's sums come from the
+  // four waves of its half.
+  auto finish_tile = [&](int t, int b) {
+    if (t + 1 < kt1) dma_wait();
+    __syncthreads();
+    if (tid < kKT) {
+      const int j = t * kKT + tid;
+      if (j < n_keys) {
+        float sum = 0.f;
+        if (split) {
+          const int w0 = (tid / (kKT / 2)) * (kWaves / 2);
+#pragma unroll
+          for (int w = 0; w < kWaves / 2; ++w) sum += sm.cs[b][w0 + w][tid];
+        } else {
+#pragma unroll
+          for (int w = 0; w < kWaves; ++w) sum += sm.cs[b][w][tid];
+        }
+        part[j] = sum;
+      }
+    }
+  };
+
+  // Tiles with frame keys (masked entries): block by block without the software
+  // pipeline, skipping the blocks past the wave's causal limit (a suffix of the
+  // tile), whose column sums are 0.
+  auto sweep2_masked_tile = [&](int t, auto nbc) {
+    constexpr int NB = decltype(nbc)::value;
+    const int b = t & 1;
+    const uint32_t kaddr = lds_addr(&sm.k[b][key0 + l32][h * 8]);
+    const uint32_t vaddr = lds_addr(&sm.v[b][key0 + tr_row][tr_col]);
+    const int first = t * kKT + key0;
+    const int na = wlim < first ? 0 : min(NB, (wlim - first) / 32 + 1);
+    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, true, std::false_type{});
+    if (active) {
+      static_for<NB>([&](auto kbc) {
+        constexpr int KB = decltype(kbc)::value;
+        const int kb = key0 / 32 + KB;  // 32-key block of the tile
+        if (KB >= na) {
+          sm.cs[b][wave][kb * 32 + key_lane] = 0.f;
+          return;
+        }
+        u32x4 kop[KS];
+        issue_k(std::integral_constant<int, KB>{}, kaddr, kop);
+        const f32x16 acc = qk_mfma(kop);
+        bf16x8 vop[2][DB];
+        static_for<2 * DB>([&](auto ic) {
+          constexpr int s_ = decltype(ic)::value / DB, db = decltype(ic)::value % DB;
+          constexpr int r0 = KB * 32 + s_ * 16;
+          const s16x4 lo = ds_read_tr<(r0 * (D + kPadV) + db * 32) * 2>(vaddr);
+          const s16x4 hi = ds_read_tr<((r0 + 8) * (D + kPadV) + db * 32) * 2>(vaddr);
+          vop[s_][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        });
+        const int rel = lim - (t * kKT + kb * 32 + 4 * h);
+        bf16x8 pe[2];
+        float cs[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          float e = fast_exp2(fmaf(acc[v], c, -mrow));
+          if (8 * (v >> 2) + (v & 3) > rel) e = 0.f;
+          pe[v >> 3][v & 7] = static_cast<__bf16>(e);
+          cs[v] = e;
+        }
+        static_for<2 * DB>([&](auto ic) {
+          constexpr int i = decltype(ic)::value, s_ = i / DB, db = i % DB;
+          lgkm_wait<2 * (2 * DB - 1 - i)>(vop[s_][db]);
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pe[s_], vop[s_][db], o[db], 0, 0, 0);
+        });
+        sm.cs[b][wave][kb * 32 + key_lane] = column_reduce(cs, lane, w0, w1);
+      });
+    } else {
+      for (int i = lane; i < kKT; i += 64) sm.cs[b][wave][i] = 0.f;
+    }
+    finish_tile(t, b);
+  };
+
+  // Tiles of state keys only (no masked entries), software-pipelined.
+  auto sweep2_tile = [&](int t, auto pure_next, auto nbc) {
     constexpr int NB = decltype(nbc)::value;
     const int b = t & 1;
     const uint32_t kaddr = lds_addr(&sm.k[b][key0 + l32][h * 8]);
@@ -513,15 +614,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
             acc_next = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kop[ks]), qreg[ks],
                                                                acc_next, 0, 0, 0);
         }
-        const int rel = lim - (t * kKT + kb * 32 + 4 * h);
         bf16x8 pe[2];
         float cs[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float e = fast_exp2(fmaf(acc[v], c, -mrow));
-          if constexpr (decltype(masked)::value) {
-            if (8 * (v >> 2) + (v & 3) > rel) e = 0.f;
-          }
+          const float e = fast_exp2(fmaf(acc[v], c, -mrow));
           pe[v >> 3][v & 7] = static_cast<__bf16>(e);
           cs[v] = e;
         }
@@ -551,33 +648,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     } else {
       for (int i = lane; i < kKT; i += 64) sm.cs[b][wave][i] = 0.f;
     }
-    if (t + 1 < kt1) dma_wait();
-    __syncthreads();
-    // cross-wave column sums of tile t -> this row tile's partials; buffer b is
-    // written again only after the next barrier.  In a split workgroup a key's
-    // sums come from the four waves of its half.
-    if (tid < kKT) {
-      const int j = t * kKT + tid;
-      if (j < n_keys) {
-        float sum = 0.f;
-        if (split) {
-          const int w0 = (tid / (kKT / 2)) * (kWaves / 2);
-#pragma unroll
-          for (int w = 0; w < kWaves / 2; ++w) sum += sm.cs[b][w0 + w][tid];
-        } else {
-#pragma unroll
-          for (int w = 0; w < kWaves; ++w) sum += sm.cs[b][w][tid];
-        }
-        part[j] = sum;
-      }
-    }
+    finish_tile(t, b);
   };
   auto sweep2 = [&](auto nbc) {
     const int tm = first_masked < kt1 ? first_masked : kt1;
-    for (int t = kt0; t + 1 < tm; ++t) sweep2_tile(t, std::false_type{}, std::true_type{}, nbc);
-    if (kt0 < tm) sweep2_tile(tm - 1, std::false_type{}, std::false_type{}, nbc);
-    for (int t = kt0 > first_masked ? kt0 : first_masked; t < kt1; ++t)
-      sweep2_tile(t, std::true_type{}, std::false_type{}, nbc);
+    for (int t = kt0; t + 1 < tm; ++t) sweep2_tile(t, std::true_type{}, nbc);
+    if (kt0 < tm) sweep2_tile(tm - 1, std::false_type{}, nbc);
+    for (int t = kt0 > first_masked ? kt0 : first_masked; t < kt1; ++t) sweep2_masked_tile(t, nbc);
   };
   if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
   dma_wait();
