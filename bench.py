@@ -652,6 +652,9 @@ def main():
     ap.add_argument("--no-baselines", action="store_true",
                     help="skip the runs reported beside the main line (whole-video curves, one-layer lines, refresh "
                          "stages, Full SA, recency window, YaRN, decode, diagnostics, the 72B-shaped stack)")
+    ap.add_argument("--layers-per-call", type=int, default=0,
+                    help="step the stack this many layers per skv_frame_step call (0: all layers in one call; "
+                         "1: the real-model calling pattern)")
     ap.add_argument("--split-refresh", action="store_true",
                     help="time the main line with the refresh as three launches (for per-stage counters)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -708,17 +711,27 @@ def main():
         for f in range(full):
             st.step(q_all[f], k_all[f], v_all[f], out)
     slots = [(i, f) for i in range(n_streams) for f in range(full, N)]
+    lpc = args.layers_per_call if 0 < args.layers_per_call < L else L
+    if L % lpc:
+        raise SystemExit(f"--layers-per-call must divide the {L} layers")
+    calls = L // lpc  # skv_frame_step calls per frame
+    views = [[(q_all[f][l:l + lpc], k_all[f][l:l + lpc], v_all[f][l:l + lpc], out[l:l + lpc], l)
+              for l in range(0, L, lpc)] for f in range(N)] if lpc < L else None
 
     def run(lo, hi):
         for i, f in slots[lo:hi]:
-            streams[i].step(q_all[f], k_all[f], v_all[f], out)
+            if views is None:
+                streams[i].step(q_all[f], k_all[f], v_all[f], out)
+            else:
+                for qq, kk, vv, oo, l in views[f]:
+                    streams[i].step(qq, kk, vv, oo, layer_begin=l, layer_count=lpc)
 
     # events for the warm-up and timed steps of every stream are created first (the host
     # takes a while, the device idles), so the warm-up steps run right before the timed ones
     recorded = slots[:args.warmup + args.steps]
     used = sorted({i for i, _ in recorded})
     for i in used:
-        streams[i].timing_start(sum(1 for j, _ in recorded if j == i))
+        streams[i].timing_start(calls * sum(1 for j, _ in recorded if j == i))
     run(0, args.warmup)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -726,8 +739,9 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     timed = slots[args.warmup:args.warmup + args.steps]
-    stages = np.concatenate([streams[i].timing_stop(args.warmup + args.steps) for i in used]).astype(np.float64)
-    stages = stages[args.warmup:]  # [K, stages] of the timed steps
+    stages = np.concatenate([streams[i].timing_stop(calls * (args.warmup + args.steps)) for i in used])
+    # [K, stages] of the timed frames (a frame's calls summed)
+    stages = stages.astype(np.float64).reshape(-1, calls, stages.shape[1]).sum(axis=1)[args.warmup:]
     # rows admitted by the last timed frame (its positions are the newest in the state)
     i_last, f_last = timed[-1]
     last_pos0 = wl.pos_offset + f_last * T
@@ -768,8 +782,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "tokens_per_frame": T, "frames_per_video": N, "capacity": wl.capacity,
-                   "layers_per_call": L, "timed_frames": f"state-full frames {full}..{N - 1} of 512-frame videos",
-                   "refresh_launches": 3 if args.split_refresh else 1,
+                   "layers_per_call": lpc, "timed_frames": f"state-full frames {full}..{N - 1} of 512-frame videos",
+                   "refresh_launches": 3 if args.split_refresh else 1, "calls_per_frame": calls,
                    "inputs": "i.i.d. N(0,1) bf16, generated in HBM"},
         "roofline": {
             "bound": "mfma",
