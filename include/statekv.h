@@ -23,7 +23,7 @@
  *   is stream-ordered; no call blocks the host except skv_timing_stop.
  * - Errors are returned as skv_status.  Argument, order and capacity errors are
  *   found before anything is enqueued and leave the context unchanged.  A launch
- *   failure (SKV_ERR_DEVICE from skv_frame_step or skv_decode_step) can come
+ *   failure (SKV_ERR_DEVICE from skv_frame_step, skv_decode_step or skv_state_view) can come
  *   after earlier kernels of the same call were enqueued: the context is then
  *   marked, and every later frame or decode step returns SKV_ERR_DEVICE until
  *   skv_reset or skv_seek restarts the stream.  Asynchronous device faults
@@ -134,6 +134,16 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
  * n * T cached tokens plus itself (causal), and only the append follows.  Layers of one frame must be stepped in order;
  * the frame counter advances after the last layer.  layer_count = n_layers
  * runs the whole stack in one launch per stage.
+ * Calls too small to fill the device (e.g. one layer of the 7B shape) split the
+ * keys of the attention over more workgroups.  When such a call covers only part
+ * of the stack, its selection and state update are not enqueued by the call
+ * itself: they run beside the attention of the next such call on other layers
+ * (the next layer of the real-model calling pattern), or are enqueued on their
+ * own by the next call that needs the state, by skv_state_view or by a context
+ * whose split_refresh is 1.  The frame's rows are read back from the decode
+ * cache for them, so k and v may be reused once the call's work is done.  The
+ * attention output, the decode-cache append and every result are the same as
+ * without the deferral.
  * Device layouts (row-major, dtype of the config):
  *   q   [layer_count][H_q ][T][d]
  *   k,v [layer_count][H_kv][T][d]
@@ -154,7 +164,9 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
  * of the 72B-shaped stack in one call; one layer per call fits).  Every call on a
  * device shares that device's array and leaves it holding its own partial
  * results; nothing in it has to start at zero.  Calls that overlap on one device
- * (contexts on different streams) race on the array: serialise them. */
+ * (contexts on different streams) race on the array: serialise them.  Since the
+ * array is reused by the next call, this entry point never defers a selection
+ * (see skv_frame_step); it enqueues one that an earlier skv_frame_step deferred. */
 skv_status skv_frame_step_noalloc(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count,
                                   const void* q, const void* k, const void* v, void* out);
 
@@ -182,7 +194,10 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
  * position.  Pointers stay valid until skv_destroy; contents change with the
  * next skv_frame_step.  The caller may write k, v, pos and score between steps
  * (used to force a given state); the first `size` slots of every KV head are
- * the state. */
+ * the state.  A selection deferred by a one-layer call (see skv_frame_step) is
+ * enqueued on the context's stream first: synchronise that stream before
+ * reading or writing through the view.  Errors: SKV_ERR_INVALID_ARG,
+ * SKV_ERR_DEVICE (that launch failed). */
 typedef struct {
   void* k;                 /* [H_kv][capacity][d] */
   void* v;                 /* [H_kv][capacity][d] */
@@ -219,13 +234,14 @@ skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* 
 /* Starts a new video on the same context: frame counter, decoded-token count
  * and L_n return to 0, every state becomes empty, and a context marked by a
  * failed launch is usable again.  Device contents are left as they are
- * (nothing is enqueued). */
+ * (nothing is enqueued; a deferred selection is dropped). */
 skv_status skv_reset(skv_ctx* ctx);
 
 /* Sets the frame counter to `frame` (0 <= frame < max_frames) at layer 0, so
  * that a caller can force a state through skv_state_view and run one step
  * from it.  The state size becomes min(B, T * frame); the decoded-token count
- * becomes 0; a context marked by a failed launch is usable again. */
+ * becomes 0; a context marked by a failed launch is usable again; a deferred
+ * selection is dropped. */
 skv_status skv_seek(skv_ctx* ctx, int64_t frame);
 
 /* Kernel timing with HIP events on the context's stream.  skv_timing_start

@@ -50,6 +50,7 @@
 // lanes, lane j points at V[k0 + j/4][d0 + 4(j%4)] and receives
 // V[k0 .. k0+3][d0 + j].
 #include "internal.h"
+#include "select.h"
 
 #include <type_traits>
 #include <utility>
@@ -179,7 +180,7 @@ __device__ inline float column_reduce(const float (&e)[16], int lane, float w0, 
 // ROPE: rotate Q at the frame tokens' virtual positions (a separate
 // instantiation, so the kernel without rotation carries none of its code).  The
 // frame's keys arrive rotated (rope_keys.hip), like the state's and the cache's.
-template <int D, bool ROPE>
+template <int D, bool ROPE, bool CARRY>
 __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = D / 16;                   // k-steps of K Q^T
   constexpr int DB = D / 32;                   // 32-column blocks of O
@@ -187,6 +188,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
 
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   Smem<D>& sm = *reinterpret_cast<Smem<D>*>(smem_raw);
+
+  // Workgroups past the plan's items carry the selection of an earlier
+  // one-layer call (an instantiation of its own for output launches that carry
+  // one; the host checks that its pool fits this workgroup's LDS).
+  if constexpr (CARRY) {
+    if (static_cast<int>(blockIdx.x) >= a.n_work) {
+      refresh_state(a.sel, static_cast<int>(blockIdx.x) - a.n_work, *reinterpret_cast<SelectShared*>(smem_raw),
+                    reinterpret_cast<uint32_t*>(smem_raw + select_lds_bytes(0)));
+      return;
+    }
+  }
 
   // The host plan fixes each workgroup's (layer, KV head), row range and
   // row-tile slot; it already places the work of one (layer, KV head) on one XCD.
@@ -730,37 +742,53 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   }
 }
 
-hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
-  const int grid = a.n_work;
-  const bool rope = a.rope_tab != nullptr;
-  if (head_dim == 128) {
-    if (rope)
-      hipLaunchKernelGGL((attn_mfma_kernel<128, true>), dim3(grid), dim3(kThreads), sizeof(Smem<128>), s, a);
-    else
-      hipLaunchKernelGGL((attn_mfma_kernel<128, false>), dim3(grid), dim3(kThreads), sizeof(Smem<128>), s, a);
-  } else {
-    if (rope)
-      hipLaunchKernelGGL((attn_mfma_kernel<64, true>), dim3(grid), dim3(kThreads), sizeof(Smem<64>), s, a);
-    else
-      hipLaunchKernelGGL((attn_mfma_kernel<64, false>), dim3(grid), dim3(kThreads), sizeof(Smem<64>), s, a);
-  }
-  return hipGetLastError();
+namespace {
+
+template <int D, bool ROPE, bool CARRY>
+void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
+  hipLaunchKernelGGL((attn_mfma_kernel<D, ROPE, CARRY>), dim3(grid), dim3(kThreads), sizeof(Smem<D>), s, a);
 }
 
-hipError_t prepare_attention_mfma() {
-  const void* kernels[] = {reinterpret_cast<const void*>(attn_mfma_kernel<128, false>),
-                            reinterpret_cast<const void*>(attn_mfma_kernel<128, true>)};
-  for (const void* k : kernels) {
-    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<128>));
-    if (e != hipSuccess) return e;
+template <int D>
+void launch_dim(const AttnArgs& a, int grid, bool rope, bool carry, hipStream_t s) {
+  if (rope) {
+    if (carry) launch_one<D, true, true>(a, grid, s);
+    else launch_one<D, true, false>(a, grid, s);
+  } else {
+    if (carry) launch_one<D, false, true>(a, grid, s);
+    else launch_one<D, false, false>(a, grid, s);
   }
-  const void* kernels64[] = {reinterpret_cast<const void*>(attn_mfma_kernel<64, false>),
-                              reinterpret_cast<const void*>(attn_mfma_kernel<64, true>)};
-  for (const void* k : kernels64) {
-    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<64>));
+}
+
+template <int D>
+hipError_t prepare_dim() {
+  const void* kernels[] = {reinterpret_cast<const void*>(attn_mfma_kernel<D, false, false>),
+                           reinterpret_cast<const void*>(attn_mfma_kernel<D, true, false>),
+                           reinterpret_cast<const void*>(attn_mfma_kernel<D, false, true>),
+                           reinterpret_cast<const void*>(attn_mfma_kernel<D, true, true>)};
+  for (const void* k : kernels) {
+    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<D>));
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
+  const bool carry = a.mode == 2 && a.n_sel > 0;
+  const int grid = a.n_work + (carry ? a.n_sel : 0);
+  const bool rope = a.rope_tab != nullptr;
+  if (head_dim == 128) launch_dim<128>(a, grid, rope, carry, s);
+  else launch_dim<64>(a, grid, rope, carry, s);
+  return hipGetLastError();
+}
+
+size_t attention_mfma_lds_bytes(int head_dim) { return head_dim == 128 ? sizeof(Smem<128>) : sizeof(Smem<64>); }
+
+hipError_t prepare_attention_mfma() {
+  const hipError_t e = prepare_dim<128>();
+  return e != hipSuccess ? e : prepare_dim<64>();
 }
 
 }  // namespace skv

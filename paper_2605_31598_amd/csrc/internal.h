@@ -9,37 +9,6 @@
 
 namespace skv {
 
-// One attention launch covers `n_layers` consecutive layers of one frame.
-// Layer indices inside the struct are relative to the first layer of the call;
-// every pointer is already offset to that layer.
-struct AttnArgs {
-  const void* q;       // [n_layers][H_q][T][d]
-  const void* kf;      // [n_layers][H_kv][T][d]   frame keys
-  const void* vf;      // [n_layers][H_kv][T][d]   frame values
-  const void* ks;      // [n_layers][H_kv][kv_rows][d]  earlier keys, rows 0..S-1 valid: the
-  const void* vs;      //   compressed state (kv_rows = B) or the decode cache (kv_rows = max_tokens)
-  void* out;           // [n_layers][H_q][T][d]
-  float* partial;      // [n_layers][H_kv][tile_stride][pool_stride] column sums of P per row
-                       // tile; null for streaming full attention (no scores)
-  const AttnWork* work;  // MFMA kernel: one work item per workgroup (n_work of them)
-  int n_work;
-  int n_layers, H_q, H_kv, G, T, B, S;
-  int kv_rows;
-  int tile_stride, pool_stride;
-  float scale_log2;    // softmax scale * log2(e)
-  const float* rope_tab;  // null: no rotation; else rotate Q by {cos, sin} per (relative position,
-                          // pair); kf holds the frame's keys already rotated
-  int rope_pos0;          // relative position of frame token 0 (n * T)
-  // Key-split plans (MFMA kernel): the launch with mode 1 writes each work
-  // item's (row max, sum of exp2) over its key range to `stats`, the launch with
-  // mode 2 merges them, writes the column sums of its key range and its fp32
-  // share of O to `opart`; workgroups of the refresh launch then add the shares.
-  int mode;               // 0: whole key range in one launch; 1: statistics; 2: output share
-  int n_ks;               // key splits of the plan (1: none)
-  float* stats;           // [n_layers * H_kv][n_ks][G * T][2]
-  float* opart;           // [n_ks][n_layers][H_q][T][d]
-};
-
 // The refresh launch finishes a frame for `n_layers` layers: score finalisation,
 // Top-B selection and state update in one workgroup per (layer, KV head), the
 // decode-cache append in a second set of workgroups of the same grid (either
@@ -79,6 +48,43 @@ struct RefreshArgs {
   const float* opart;        // [n_ks][out_elems]
   void* out;                 // [out_elems] bf16
   int64_t out_elems;         // a multiple of 4
+};
+
+// One attention launch covers `n_layers` consecutive layers of one frame.
+// Layer indices inside the struct are relative to the first layer of the call;
+// every pointer is already offset to that layer.
+struct AttnArgs {
+  const void* q;       // [n_layers][H_q][T][d]
+  const void* kf;      // [n_layers][H_kv][T][d]   frame keys
+  const void* vf;      // [n_layers][H_kv][T][d]   frame values
+  const void* ks;      // [n_layers][H_kv][kv_rows][d]  earlier keys, rows 0..S-1 valid: the
+  const void* vs;      //   compressed state (kv_rows = B) or the decode cache (kv_rows = max_tokens)
+  void* out;           // [n_layers][H_q][T][d]
+  float* partial;      // [n_layers][H_kv][tile_stride][pool_stride] column sums of P per row
+                       // tile; null for streaming full attention (no scores)
+  const AttnWork* work;  // MFMA kernel: one work item per workgroup (n_work of them)
+  int n_work;
+  int n_layers, H_q, H_kv, G, T, B, S;
+  int kv_rows;
+  int tile_stride, pool_stride;
+  float scale_log2;    // softmax scale * log2(e)
+  const float* rope_tab;  // null: no rotation; else rotate Q by {cos, sin} per (relative position,
+                          // pair); kf holds the frame's keys already rotated
+  int rope_pos0;          // relative position of frame token 0 (n * T)
+  // Key-split plans (MFMA kernel): the launch with mode 1 writes each work
+  // item's (row max, sum of exp2) over its key range to `stats`, the launch with
+  // mode 2 merges them, writes the column sums of its key range and its fp32
+  // share of O to `opart`; workgroups of the refresh launch then add the shares.
+  int mode;               // 0: whole key range in one launch; 1: statistics; 2: output share
+  int n_ks;               // key splits of the plan (1: none)
+  float* stats;           // [n_layers * H_kv][n_ks][G * T][2]
+  float* opart;           // [n_ks][n_layers][H_q][T][d]
+  // An output launch (mode 2) can carry the selection of an earlier one-layer
+  // call: n_sel more workgroups, one per (layer, KV head) of `sel`, finalise its
+  // scores, select and update its state, with the frame's rows read back from
+  // the decode cache, where that call appended them.
+  int n_sel;
+  RefreshArgs sel;
 };
 
 // Decode over the detailed cache (split-key flash decoding).  Each wave of the
@@ -131,5 +137,9 @@ hipError_t launch_refresh_append(const RefreshArgs& a, hipStream_t s);
 hipError_t launch_rope_keys(const void* in, void* out, int n_blocks, int t, int row_bytes, int elem,
                             const float* tab, int pos0, hipStream_t s);
 hipError_t prepare_kernels(int head_dim, bool bf16, int pool_stride);
+// LDS bytes of an MFMA attention workgroup (what a carried selection may use).
+size_t attention_mfma_lds_bytes(int head_dim);
+// LDS bytes a selection workgroup needs for a pool of P candidates.
+size_t selection_lds_bytes(int P);
 
 }  // namespace skv

@@ -103,6 +103,12 @@ struct skv_ctx {
   int dec_next_layer = 0;  // next layer expected within the current decode call
   int dec_pending = 0;     // tokens of the decode call in progress
   std::vector<int32_t> last_pool;  // candidates of each layer's last step
+  // A one-layer call's selection and state update, left to the output launch of
+  // the next one-layer call on other layers (pend_ra: its refresh arguments,
+  // reading the frame's rows back from the decode cache).
+  bool pend = false;
+  int pend_lb = 0, pend_lc = 0;
+  skv::RefreshArgs pend_ra{};
 
   // timing
   std::vector<hipEvent_t> events;  // (SKV_N_STAGES + 1) per recorded step
@@ -273,6 +279,7 @@ hipError_t scratch_address(int device, void** out) {
 
 // Per-call buffers of a frame step.
 struct StepScratch {
+  bool own_layers;      // partial and admit lists are per layer (their contents outlive the call)
   float* partial;       // [layer_count * H_kv][tile_stride][pool_stride]
   float* split_stats;   // [layer_count * H_kv][n_ks][G * T][2]
   float* split_out;     // [n_ks][layer_count][H_q][T][d]
@@ -447,6 +454,14 @@ skv_status check_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_cou
 
 // Scratch bytes a frame step of layer_count layers needs (each buffer 256-byte aligned),
 // and the buffers carved from `base` when base is not null.
+// Enqueues, as a launch of its own, the selection a one-layer call left for a
+// later output launch (if any).
+hipError_t flush_pending(skv_ctx* ctx) {
+  if (!ctx->pend) return hipSuccess;
+  ctx->pend = false;
+  return skv::launch_refresh(ctx->pend_ra, ctx->stream);
+}
+
 size_t carve_scratch(const skv_ctx* ctx, int32_t layer_count, char* base, StepScratch* sc) {
   const skv_config& c = ctx->cfg;
   const size_t LH = static_cast<size_t>(layer_count) * c.n_kv_heads;
@@ -467,6 +482,7 @@ size_t carve_scratch(const skv_ctx* ctx, int32_t layer_count, char* base, StepSc
     off += (sizes[i] + 255) / 256 * 256;
   }
   if (sc != nullptr) {
+    sc->own_layers = false;
     sc->partial = static_cast<float*>(ptrs[0]);
     sc->split_stats = static_cast<float*>(ptrs[1]);
     sc->split_out = static_cast<float*>(ptrs[2]);
@@ -502,7 +518,7 @@ skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_c
   // with RoPE every later reader takes the frame's keys rotated (launched first below)
   const void* k_used = ctx->rope_tab != nullptr ? ctx->rope_keys : k;
 
-  skv::AttnArgs aa;
+  skv::AttnArgs aa{};
   aa.q = q;
   aa.kf = k_used;
   aa.vf = v;
@@ -538,7 +554,7 @@ skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_c
   aa.stats = sc.split_stats;
   aa.opart = sc.split_out;
 
-  skv::RefreshArgs ra;
+  skv::RefreshArgs ra{};
   ra.partial = aa.partial;
   ra.lg_tiles = plan.tiles;
   ra.tile_stride = ctx->tile_stride;
@@ -576,9 +592,26 @@ skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_c
   ra.opart = sc.split_out;
   ra.out = out;
   ra.out_elems = static_cast<int64_t>(layer_count) * c.n_q_heads * T * d;
-  ra.n_comb = static_cast<int>(std::min<int64_t>(128, (ra.out_elems / 4 + skv::kSelectThreads - 1) / skv::kSelectThreads));
+  // one group of four output values per combine thread; beside selection
+  // workgroups at most 128 combine workgroups, which leave the memory system to
+  // the selections' latency-bound loads
+  const int64_t comb_wgs = (ra.out_elems / 4 + skv::kSelectThreads - 1) / skv::kSelectThreads;
 
-  hipError_t e = mark(0);
+  // A key-split call of a multi-layer context (one layer of the real-model calling
+  // pattern) leaves its selection and state update to the output launch of the
+  // next such call on other layers, where they run beside that call's attention
+  // instead of after the output sum; that call carries it (or, when none does,
+  // the next use of the state enqueues it on its own).  The frame's rows are
+  // then read back from the decode cache, since the caller's k and v may be
+  // reused once this call's work is done.
+  const bool key_split = ctx->use_mfma && !full && plan.n_ks > 1;
+  const bool defer = key_split && sc.own_layers && !c.split_refresh && layer_count < c.n_layers &&
+                     skv::selection_lds_bytes(S + T) <= skv::attention_mfma_lds_bytes(d);
+  const bool carry = ctx->pend && key_split &&
+                     (ctx->pend_lb + ctx->pend_lc <= layer_begin || layer_begin + layer_count <= ctx->pend_lb);
+  ra.n_comb = static_cast<int>(std::min<int64_t>(defer ? 1024 : 128, comb_wgs));
+  hipError_t e = ctx->pend && !carry ? flush_pending(ctx) : hipSuccess;
+  if (e == hipSuccess) e = mark(0);
   if (e == hipSuccess && ctx->rope_tab != nullptr)
     e = skv::launch_rope_keys(k, ctx->rope_keys, layer_count * Hkv, T, static_cast<int>(rb), ctx->elem, ctx->rope_tab,
                               static_cast<int>(ctx->frame * T), ctx->stream);
@@ -591,7 +624,12 @@ skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_c
       aa.mode = 1;
       e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
       aa.mode = 2;
+      if (carry) {
+        aa.n_sel = ctx->pend_lc * Hkv;
+        aa.sel = ctx->pend_ra;
+      }
       if (e == hipSuccess) e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+      if (e == hipSuccess && carry) ctx->pend = false;
     } else {
       e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
     }
@@ -607,6 +645,21 @@ skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_c
     if (e == hipSuccess && !full) e = skv::launch_refresh_update(ra, ctx->stream);
     if (e == hipSuccess) e = mark(3);
     if (e == hipSuccess) e = skv::launch_refresh_append(ra, ctx->stream);
+  } else if (defer) {
+    skv::RefreshArgs now = ra;  // the output sum and the append; the selection waits
+    now.select = false;
+    if (e == hipSuccess) e = skv::launch_refresh(now, ctx->stream);
+    if (e == hipSuccess) {
+      ctx->pend_ra = ra;
+      ctx->pend_ra.append = false;
+      ctx->pend_ra.n_ks = 1;
+      ctx->pend_ra.kf = static_cast<const char*>(ra.ck) + static_cast<size_t>(ra.first_row) * rb;
+      ctx->pend_ra.vf = static_cast<const char*>(ra.cv) + static_cast<size_t>(ra.first_row) * rb;
+      ctx->pend_ra.kf_rows = ctx->max_tokens;
+      ctx->pend_lb = layer_begin;
+      ctx->pend_lc = layer_count;
+      ctx->pend = true;
+    }
   } else {
     if (e == hipSuccess) e = skv::launch_refresh(ra, ctx->stream);
   }
@@ -637,6 +690,7 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
   const skv_config& c = ctx->cfg;
   const size_t lh0 = static_cast<size_t>(layer_begin) * c.n_kv_heads;
   StepScratch sc;
+  sc.own_layers = true;
   sc.partial = ctx->partial != nullptr ? ctx->partial + lh0 * ctx->tile_stride * ctx->pool_stride : nullptr;
   sc.split_stats = ctx->split_stats;
   sc.split_out = ctx->split_out;
@@ -777,6 +831,13 @@ skv_status skv_state_view(skv_ctx* ctx, int32_t layer, skv_state_view_t* out) {
   const skv_config& c = ctx->cfg;
   if (layer < 0 || layer >= c.n_layers) return fail(SKV_ERR_INVALID_ARG, "layer out of range");
   const size_t lh = static_cast<size_t>(layer) * c.n_kv_heads;
+  if (ctx->pend) {  // a deferred selection is enqueued before anyone reads the state
+    const hipError_t e = flush_pending(ctx);
+    if (e != hipSuccess) {
+      ctx->broken = true;
+      return hip_fail(e, "deferred selection launch");
+    }
+  }
   const int done = layer_frames_done(ctx, layer);
   out->k = static_cast<char*>(ctx->state_k) + lh * c.capacity * ctx->row_bytes;
   out->v = static_cast<char*>(ctx->state_v) + lh * c.capacity * ctx->row_bytes;
@@ -811,6 +872,7 @@ skv_status skv_decode_cache_view(skv_ctx* ctx, int32_t layer, skv_cache_view_t* 
 skv_status skv_reset(skv_ctx* ctx) {
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
   ctx->broken = false;
+  ctx->pend = false;  // the state starts empty; a deferred selection is void
   ctx->frame = 0;
   ctx->next_layer = 0;
   ctx->n_decoded = 0;
@@ -824,6 +886,7 @@ skv_status skv_seek(skv_ctx* ctx, int64_t frame) {
   if (ctx == nullptr) return fail(SKV_ERR_INVALID_ARG, "ctx is NULL");
   if (frame < 0 || frame >= ctx->cfg.max_frames) return fail(SKV_ERR_INVALID_ARG, "frame out of range");
   ctx->broken = false;
+  ctx->pend = false;  // the state is the caller's to set; a deferred selection is void
   ctx->frame = frame;
   ctx->next_layer = 0;
   ctx->n_decoded = 0;

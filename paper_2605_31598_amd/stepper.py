@@ -98,8 +98,8 @@ class FrameStepper:
 
     def read_state(self, layer):
         """Host copy of one layer's compressed state and last candidate pool."""
+        sv = B.skv_state_view(self.ctx, layer)  # enqueues a deferred selection, if any
         self._sync()
-        sv = B.skv_state_view(self.ctx, layer)
         H, cap, d, n = self.H_kv, self.B, self.d, sv.size
         kb = B.copy_to_host(sv.k, H * cap * d * self.elem).view(self.np_dtype).reshape(H, cap, d)
         vb = B.copy_to_host(sv.v, H * cap * d * self.elem).view(self.np_dtype).reshape(H, cap, d)
@@ -114,8 +114,8 @@ class FrameStepper:
 
     def write_state(self, layer, pos, k, v, score=None):
         """Overwrite slots 0..n-1 of every KV head (n = pos.shape[1]) to force a state."""
+        sv = B.skv_state_view(self.ctx, layer)  # enqueues a deferred selection, if any
         self._sync()
-        sv = B.skv_state_view(self.ctx, layer)
         H, cap, d = self.H_kv, self.B, self.d
         n = pos.shape[1]
         if n != sv.size:
