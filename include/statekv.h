@@ -113,6 +113,13 @@ typedef struct {
                                another); 1: three launches, selection, state update, append, so that each
                                stage can be timed (skv_timing_*) and profiled on its own.  The results
                                are the same bit for bit. */
+  int32_t key_split_mode;   /* calls too small to fill the device split the attention's keys into ranges
+                               whose row statistics are merged before the output: 0 (a zeroed config):
+                               one launch, in which the workgroups of a row range exchange their ranges'
+                               statistics (each waits a bounded time for the others and computes any
+                               that has not arrived); 1: two launches, statistics then output; 2: one
+                               launch in which every workgroup computes every range's statistics itself.
+                               The results are the same bit for bit. */
 } skv_config;
 
 typedef struct skv_ctx skv_ctx;
@@ -121,8 +128,8 @@ typedef struct skv_ctx skv_ctx;
  * (compressed state and decode cache of all layers, scratch), and binds the
  * context to hip_stream (a hipStream_t; NULL means the default stream).
  * Limits: pos_offset + max_frames * T + max_decode_tokens < 2^31; B + T <= 16384
- * (STATEKV and RECENT); policy one of skv_policy and split_refresh 0 or 1, else
- * SKV_ERR_INVALID_ARG.
+ * (STATEKV and RECENT); policy one of skv_policy, split_refresh 0 or 1 and
+ * key_split_mode 0, 1 or 2, else SKV_ERR_INVALID_ARG.
  * Returns SKV_OK and *out, or an error and *out = NULL. */
 skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out);
 

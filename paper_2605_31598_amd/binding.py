@@ -53,6 +53,7 @@ class skv_config(ctypes.Structure):
         ("pos_offset", ctypes.c_int64), ("policy", ctypes.c_int32), ("max_decode_tokens", ctypes.c_int32),
         ("rope", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("rope_factor", ctypes.c_float),
         ("rope_orig_max", ctypes.c_int32), ("split_refresh", ctypes.c_int32),
+        ("key_split_mode", ctypes.c_int32),
     ]
 
 

@@ -180,7 +180,7 @@ __device__ inline float column_reduce(const float (&e)[16], int lane, float w0, 
 // ROPE: rotate Q at the frame tokens' virtual positions (a separate
 // instantiation, so the kernel without rotation carries none of its code).  The
 // frame's keys arrive rotated (rope_keys.hip), like the state's and the cache's.
-template <int D, bool ROPE, bool CARRY>
+template <int D, bool ROPE, int VAR>
 __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KS = D / 16;                   // k-steps of K Q^T
   constexpr int DB = D / 32;                   // 32-column blocks of O
@@ -190,9 +190,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   Smem<D>& sm = *reinterpret_cast<Smem<D>*>(smem_raw);
 
   // Workgroups past the plan's items carry the selection of an earlier
-  // one-layer call (an instantiation of its own for output launches that carry
+  // one-layer call (instantiations of their own for the launches that can carry
   // one; the host checks that its pool fits this workgroup's LDS).
-  if constexpr (CARRY) {
+  if constexpr (VAR != 0) {
     if (static_cast<int>(blockIdx.x) >= a.n_work) {
       refresh_state(a.sel, static_cast<int>(blockIdx.x) - a.n_work, *reinterpret_cast<SelectShared*>(smem_raw),
                     reinterpret_cast<uint32_t*>(smem_raw + select_lds_bytes(0)));
@@ -215,8 +215,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   const int first_masked = S / kKT;  // tiles from here on contain frame keys or the ragged end
   // key tiles of this work item: all, or its share [kt0, kt1) of a key-split plan
   const int ks = wk.ks;
-  const int kt0 = static_cast<int>(static_cast<int64_t>(ks) * n_tiles / a.n_ks);
-  const int kt1 = static_cast<int>(static_cast<int64_t>(ks + 1) * n_tiles / a.n_ks);
+  auto range_lo = [&](int r) { return static_cast<int>(static_cast<int64_t>(r) * n_tiles / a.n_ks); };
+  int kt0 = range_lo(ks), kt1 = range_lo(ks + 1);  // reassigned only by a fused key split's fallback
   const int row_end = wk.row0 + wk.rows;  // rows of this workgroup: [wk.row0, row_end)
   // split workgroup: waves w and w + 4 take the same 32 rows, the first and the
   // second half of every key tile
@@ -447,39 +447,130 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     mrow = row_valid ? mm * c : 0.f;
     inv_l = row_valid ? 1.0f / ll : 0.f;
   } else {
-    if (kt0 < kt1) dma_tile(kt0, kt0 & 1, false, std::false_type{});
-    dma_wait();
-    __syncthreads();
-    if (split)
-      sweep1(std::integral_constant<int, kKT / 64>{});
-    else
-      sweep1(std::integral_constant<int, kKT / 32>{});
+    // sweep 1 over key tiles [kt0, kt1): this range's (max, sum) per row, in mm, ll
+    float mm, ll;
+    auto row_stats = [&]() {
+      m = -1e30f;
+      l = 0.f;
+      if (kt0 < kt1) dma_tile(kt0, kt0 & 1, false, std::false_type{});
+      dma_wait();
+      __syncthreads();
+      if (split)
+        sweep1(std::integral_constant<int, kKT / 64>{});
+      else
+        sweep1(std::integral_constant<int, kKT / 32>{});
 
-    // The other 16 keys of every 32-key block live in lane ^ 32.  Both lanes merge
-    // in one operand order (h = 0's statistics first; the merge rounds differently
-    // with the operands swapped), so the two lanes of a row hold bit-identical
-    // statistics and equal keys get equal column sums wherever they sit in a block.
-    const float mo = __shfl_xor(m, 32, 64);
-    const float lo = __shfl_xor(l, 32, 64);
-    const float ma = h ? mo : m, la = h ? lo : l, mb = h ? m : mo, lb = h ? l : lo;
-    float mm = fmaxf(ma, mb);
-    float ll = la * fast_exp2((ma - mm) * c) + lb * fast_exp2((mb - mm) * c);
-    if (split) {
-      // the other key half of these rows is wave ^ 4's; exchanged through the
-      // second column-sum buffer, first written after sweep 2's first barrier;
-      // merged with the first half's statistics first in both waves
-      float* xm = &sm.cs[1][wave][0];
-      if (h == 0) {
-        xm[l32] = mm;
-        xm[32 + l32] = ll;
+      // The other 16 keys of every 32-key block live in lane ^ 32.  Both lanes merge
+      // in one operand order (h = 0's statistics first; the merge rounds differently
+      // with the operands swapped), so the two lanes of a row hold bit-identical
+      // statistics and equal keys get equal column sums wherever they sit in a block.
+      const float mo = __shfl_xor(m, 32, 64);
+      const float lo = __shfl_xor(l, 32, 64);
+      const float ma = h ? mo : m, la = h ? lo : l, mb = h ? m : mo, lb = h ? l : lo;
+      mm = fmaxf(ma, mb);
+      ll = la * fast_exp2((ma - mm) * c) + lb * fast_exp2((mb - mm) * c);
+      if (split) {
+        // the other key half of these rows is wave ^ 4's; exchanged through the
+        // second column-sum buffer, first written after sweep 2's first barrier;
+        // merged with the first half's statistics first in both waves
+        float* xm = &sm.cs[1][wave][0];
+        if (h == 0) {
+          xm[l32] = mm;
+          xm[32 + l32] = ll;
+        }
+        __syncthreads();
+        const float* pm = &sm.cs[1][wave ^ 4][0];
+        const float mp = pm[l32], lp = pm[32 + l32];
+        const float m0 = grp ? mp : mm, l0 = grp ? lp : ll, m1 = grp ? mm : mp, l1 = grp ? ll : lp;
+        const float mt = fmaxf(m0, m1);
+        ll = l0 * fast_exp2((m0 - mt) * c) + l1 * fast_exp2((m1 - mt) * c);
+        mm = mt;
+      }
+    };
+    row_stats();
+    if constexpr (VAR == 2) {
+      // Fused key split (mode 3): the workgroups of one row range exchange their
+      // ranges' statistics through `stats` instead of ending the launch.  Each
+      // publishes its own (device-scope stores, then its flag = this launch's
+      // epoch), waits for the others' flags for at most wait_ticks of the
+      // constant clock, and computes every range still missing itself: sweep 1
+      // over that range gives bit for bit what its own workgroup publishes, so
+      // the result never depends on who computed what, and every wait ends.
+      // Mode 4 waits for nobody (every workgroup computes every range).
+      const int GT = a.G * a.T;
+      auto publish = [&](int r) {
+        if (h == 0 && grp == 0 && row_valid) {
+          uint32_t* st = reinterpret_cast<uint32_t*>(stats + (static_cast<size_t>(r) * GT + r_lane) * 2);
+          __hip_atomic_store(st, __float_as_uint(mm), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(st + 1, __float_as_uint(ll), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's stores have completed
+      };
+      publish(ks);
+      __syncthreads();  // every wave's stores have completed; the tile buffers are free
+      // sweep 2's first tile is copied while the workgroup waits for the others
+      if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
+      const unsigned all = (1u << a.n_ks) - 1u;
+      unsigned* shared_mask = reinterpret_cast<unsigned*>(&sm.il[0][0]);  // free until the epilogue
+      if (tid == 0) {
+        uint32_t* flags = a.flags + (static_cast<size_t>(lg) * a.tile_stride + wk.tile) * a.n_ks;
+        unsigned got = 1u << ks;
+        if (a.mode == 3) {
+          __hip_atomic_store(&flags[ks], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const uint64_t t_end = __builtin_amdgcn_s_memrealtime() + a.wait_ticks;
+          for (;;) {
+            for (int r = 0; r < a.n_ks; ++r)
+              if (!(got >> r & 1u) && __hip_atomic_load(&flags[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.epoch)
+                got |= 1u << r;
+            if (got == all || __builtin_amdgcn_s_memrealtime() > t_end) break;
+            __builtin_amdgcn_s_sleep(2);
+          }
+        }
+        *shared_mask = got;
       }
       __syncthreads();
-      const float* pm = &sm.cs[1][wave ^ 4][0];
-      const float mp = pm[l32], lp = pm[32 + l32];
-      const float m0 = grp ? mp : mm, l0 = grp ? lp : ll, m1 = grp ? mm : mp, l1 = grp ? ll : lp;
-      const float mt = fmaxf(m0, m1);
-      ll = l0 * fast_exp2((m0 - mt) * c) + l1 * fast_exp2((m1 - mt) * c);
-      mm = mt;
+      unsigned todo = all & ~*shared_mask;
+      const bool refill = todo != 0u;
+      if (refill) {  // the tile buffers are needed: the copy above lands first
+        dma_wait();
+        __syncthreads();
+      }
+      while (todo != 0u) {  // ranges whose statistics did not arrive in time
+        const int r = __builtin_ctz(todo);
+        todo &= todo - 1u;
+        kt0 = range_lo(r);
+        kt1 = range_lo(r + 1);
+        row_stats();
+        publish(r);
+      }
+      kt0 = range_lo(ks);
+      kt1 = range_lo(ks + 1);
+      if (refill && kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
+      __syncthreads();  // the ranges computed here are in `stats` before anyone reads them
+      // merge every range's statistics in split order (as the output launch of
+      // the two-launch scheme does)
+      float mg = -1e30f, lg_sum = 0.f;
+      if (row_valid) {
+        float ms[kMaxKeySplits], lsum[kMaxKeySplits];
+#pragma unroll
+        for (int r = 0; r < kMaxKeySplits; ++r) {
+          ms[r] = -1e30f;
+          lsum[r] = 0.f;
+          if (r < a.n_ks) {
+            const uint32_t* st = reinterpret_cast<const uint32_t*>(stats + (static_cast<size_t>(r) * GT + r_lane) * 2);
+            ms[r] = __uint_as_float(__hip_atomic_load(st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            lsum[r] = __uint_as_float(__hip_atomic_load(st + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < kMaxKeySplits; ++r) {
+          const float mt = fmaxf(mg, ms[r]);
+          lg_sum = lg_sum * fast_exp2((mg - mt) * c) + lsum[r] * fast_exp2((ms[r] - mt) * c);
+          mg = mt;
+        }
+      }
+      mm = mg;
+      ll = lg_sum;
     }
     if (a.mode == 1) {
       // statistics launch of a key-split plan: this key range's (max, sum) per row
@@ -668,7 +759,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (kt0 < tm) sweep2_tile(tm - 1, std::false_type{}, nbc);
     for (int t = kt0 > first_masked ? kt0 : first_masked; t < kt1; ++t) sweep2_masked_tile(t, nbc);
   };
-  if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
+  if constexpr (VAR != 2) {  // a fused key split issued this copy before its wait
+    if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
+  }
   dma_wait();
   __syncthreads();
   if (split)
@@ -700,7 +793,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   // ---------------- output: O / sum, staged through LDS for 16-byte stores ----------------
   if (writer && h == 0) sm.il[wave][l32] = inv_l;
   __syncthreads();
-  if (a.mode == 2) {
+  if (a.mode >= 2) {
     // this key range's share of O (already divided by the merged sum), fp32
     if (writer) {
       float* op = a.opart + static_cast<size_t>(ks) * a.n_layers * a.H_q * a.T * D +
@@ -744,28 +837,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
 
 namespace {
 
-template <int D, bool ROPE, bool CARRY>
+template <int D, bool ROPE, int VAR>
 void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL((attn_mfma_kernel<D, ROPE, CARRY>), dim3(grid), dim3(kThreads), sizeof(Smem<D>), s, a);
+  hipLaunchKernelGGL((attn_mfma_kernel<D, ROPE, VAR>), dim3(grid), dim3(kThreads), sizeof(Smem<D>), s, a);
 }
 
-template <int D>
-void launch_dim(const AttnArgs& a, int grid, bool rope, bool carry, hipStream_t s) {
-  if (rope) {
-    if (carry) launch_one<D, true, true>(a, grid, s);
-    else launch_one<D, true, false>(a, grid, s);
-  } else {
-    if (carry) launch_one<D, false, true>(a, grid, s);
-    else launch_one<D, false, false>(a, grid, s);
-  }
+template <int D, bool ROPE>
+void launch_var(const AttnArgs& a, int grid, int var, hipStream_t s) {
+  if (var == 2) launch_one<D, ROPE, 2>(a, grid, s);
+  else if (var == 1) launch_one<D, ROPE, 1>(a, grid, s);
+  else launch_one<D, ROPE, 0>(a, grid, s);
 }
 
 template <int D>
 hipError_t prepare_dim() {
-  const void* kernels[] = {reinterpret_cast<const void*>(attn_mfma_kernel<D, false, false>),
-                           reinterpret_cast<const void*>(attn_mfma_kernel<D, true, false>),
-                           reinterpret_cast<const void*>(attn_mfma_kernel<D, false, true>),
-                           reinterpret_cast<const void*>(attn_mfma_kernel<D, true, true>)};
+  const void* kernels[] = {
+      reinterpret_cast<const void*>(attn_mfma_kernel<D, false, 0>), reinterpret_cast<const void*>(attn_mfma_kernel<D, true, 0>),
+      reinterpret_cast<const void*>(attn_mfma_kernel<D, false, 1>), reinterpret_cast<const void*>(attn_mfma_kernel<D, true, 1>),
+      reinterpret_cast<const void*>(attn_mfma_kernel<D, false, 2>), reinterpret_cast<const void*>(attn_mfma_kernel<D, true, 2>)};
   for (const void* k : kernels) {
     const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, sizeof(Smem<D>));
     if (e != hipSuccess) return e;
@@ -776,11 +865,20 @@ hipError_t prepare_dim() {
 }  // namespace
 
 hipError_t launch_attention_mfma_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
-  const bool carry = a.mode == 2 && a.n_sel > 0;
-  const int grid = a.n_work + (carry ? a.n_sel : 0);
+  // instantiation: 2 = fused key split (modes 3, 4), 1 = output launch carrying a
+  // selection, 0 = everything else; the first two can carry a selection
+  const bool fused = a.mode == 3 || a.mode == 4;
+  const int var = fused ? 2 : (a.mode == 2 && a.n_sel > 0 ? 1 : 0);
+  const int grid = a.n_work + (var != 0 ? a.n_sel : 0);
+  if (fused && (a.flags == nullptr || a.n_ks > kMaxKeySplits)) return hipErrorInvalidValue;
   const bool rope = a.rope_tab != nullptr;
-  if (head_dim == 128) launch_dim<128>(a, grid, rope, carry, s);
-  else launch_dim<64>(a, grid, rope, carry, s);
+  if (head_dim == 128) {
+    if (rope) launch_var<128, true>(a, grid, var, s);
+    else launch_var<128, false>(a, grid, var, s);
+  } else {
+    if (rope) launch_var<64, true>(a, grid, var, s);
+    else launch_var<64, false>(a, grid, var, s);
+  }
   return hipGetLastError();
 }
 

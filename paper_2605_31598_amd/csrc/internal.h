@@ -75,10 +75,18 @@ struct AttnArgs {
   // item's (row max, sum of exp2) over its key range to `stats`, the launch with
   // mode 2 merges them, writes the column sums of its key range and its fp32
   // share of O to `opart`; workgroups of the refresh launch then add the shares.
-  int mode;               // 0: whole key range in one launch; 1: statistics; 2: output share
+  // Modes 3 and 4 do both in one launch: the workgroups of one row range
+  // exchange their ranges' statistics through `stats` and per-item flags set to
+  // `epoch` (mode 3, waiting at most wait_ticks of the constant clock for each
+  // other and computing what has not arrived), or each computes every range
+  // itself (mode 4).  The output, shares and column sums equal the two launches'.
+  int mode;               // 0: whole key range in one launch; 1: statistics; 2: output share; 3, 4: both
   int n_ks;               // key splits of the plan (1: none)
   float* stats;           // [n_layers * H_kv][n_ks][G * T][2]
   float* opart;           // [n_ks][n_layers][H_q][T][d]
+  uint32_t* flags;        // modes 3, 4: [n_layers * H_kv][tile_stride][n_ks], zero or an earlier epoch
+  uint32_t epoch;         // nonzero, different from every earlier launch's on the same flags
+  uint64_t wait_ticks;
   // An output launch (mode 2) can carry the selection of an earlier one-layer
   // call: n_sel more workgroups, one per (layer, KV head) of `sel`, finalise its
   // scores, select and update its state, with the frame's rows read back from

@@ -90,6 +90,9 @@ struct skv_ctx {
     int n_ks = 1;                    // key splits (calls too small to fill the device)
   };
   std::vector<Plan> plans;
+  uint32_t* ks_flags = nullptr;    // fused key-split launches: per-item flags, [L][H_kv][tile_stride][16]
+  uint32_t ks_epoch = 0;           // the last such launch's epoch
+  uint64_t ks_wait_ticks = 0;      // how long their workgroups wait for each other (constant clock)
   float* split_stats = nullptr;    // key-split plans: per-range row statistics and output shares,
   float* split_out = nullptr;      // sized for the largest such plan (null if none)
   void* scratch = nullptr;         // this device's static scratch (skv_frame_step_noalloc)
@@ -246,6 +249,17 @@ skv_status build_plans(skv_ctx* c, int rows) {
     if (s != SKV_OK) return s;
     s = alloc(c, out_floats * sizeof(float), reinterpret_cast<void**>(&c->split_out));
     if (s != SKV_OK) return s;
+    const size_t flag_bytes = static_cast<size_t>(cfg.n_layers) * cfg.n_kv_heads * c->tile_stride * skv::kMaxKeySplits *
+                              sizeof(uint32_t);
+    s = alloc(c, flag_bytes, reinterpret_cast<void**>(&c->ks_flags));
+    if (s != SKV_OK) return s;
+    hipError_t e = hipMemsetAsync(c->ks_flags, 0, flag_bytes, c->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    // the workgroups of a fused key-split launch wait at most 200 us for each other
+    int khz = 0;
+    e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->device);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    c->ks_wait_ticks = static_cast<uint64_t>(khz > 0 ? khz : 100000) * 200 / 1000;
   }
   return SKV_OK;
 }
@@ -334,6 +348,7 @@ skv_status skv_init(const skv_config* cfg, void* hip_stream, skv_ctx** out) {
   if (c.policy != SKV_POLICY_STATEKV && c.policy != SKV_POLICY_RECENT && c.policy != SKV_POLICY_FULL)
     return fail(SKV_ERR_INVALID_ARG, "unknown policy");
   if (c.split_refresh != 0 && c.split_refresh != 1) return fail(SKV_ERR_INVALID_ARG, "split_refresh must be 0 or 1");
+  if (c.key_split_mode < 0 || c.key_split_mode > 2) return fail(SKV_ERR_INVALID_ARG, "key_split_mode must be 0, 1 or 2");
   const bool full = c.policy == SKV_POLICY_FULL;
   if (!full && static_cast<int64_t>(c.capacity) + c.tokens_per_frame > skv::kMaxPool)
     return fail(SKV_ERR_UNSUPPORTED, "capacity + tokens_per_frame exceeds 16384");
@@ -620,15 +635,24 @@ skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_c
       e = skv::launch_attention_simple_f32(aa, d, ctx->stream);
     } else if (full) {
       e = skv::launch_attention_full_bf16(aa, d, ctx->stream);
-    } else if (plan.n_ks > 1) {  // key-split plan: statistics, output shares, their sum
-      aa.mode = 1;
-      e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
-      aa.mode = 2;
+    } else if (plan.n_ks > 1) {  // key-split plan: statistics and output shares (their sum below)
       if (carry) {
         aa.n_sel = ctx->pend_lc * Hkv;
         aa.sel = ctx->pend_ra;
       }
-      if (e == hipSuccess) e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+      if (c.key_split_mode == 1) {  // two launches
+        aa.mode = 1;
+        e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+        aa.mode = 2;
+        if (e == hipSuccess) e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+      } else {  // one launch; its workgroups exchange the statistics (mode 3) or each computes all (4)
+        aa.mode = c.key_split_mode == 2 ? 4 : 3;
+        aa.flags = ctx->ks_flags;
+        aa.epoch = ++ctx->ks_epoch;
+        if (aa.epoch == 0u) aa.epoch = ++ctx->ks_epoch;  // 0 is the flags' initial value
+        aa.wait_ticks = ctx->ks_wait_ticks;
+        e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);
+      }
       if (e == hipSuccess && carry) ctx->pend = false;
     } else {
       e = skv::launch_attention_mfma_bf16(aa, d, ctx->stream);

@@ -20,7 +20,7 @@ class FrameStepper:
     def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
                  dtype="bf16", softmax_scale=0.0, pos_offset=0, stream=None, policy="statekv",
                  max_decode_tokens=0, rope=None, rope_theta=0.0, rope_factor=1.0, rope_orig_max=0,
-                 split_refresh=False):
+                 split_refresh=False, key_split_mode=0):
         import torch
 
         if not torch.cuda.is_available():
@@ -35,7 +35,7 @@ class FrameStepper:
         self.cfg = B.skv_config(n_layers, n_q_heads, n_kv_heads, head_dim, tokens_per_frame, capacity, max_frames,
                                 _DTYPES[dtype], softmax_scale, pos_offset, B.POLICIES[policy], max_decode_tokens,
                                 {None: B.SKV_ROPE_NONE, "plain": B.SKV_ROPE_PLAIN, "yarn": B.SKV_ROPE_YARN}[rope],
-                                rope_theta, rope_factor, rope_orig_max, int(bool(split_refresh)))
+                                rope_theta, rope_factor, rope_orig_max, int(bool(split_refresh)), int(key_split_mode))
         self.n_layers, self.H_q, self.H_kv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         # streaming full attention keeps no compressed state
         self.T, self.B, self.max_frames = tokens_per_frame, (0 if policy == "full" else capacity), max_frames

@@ -55,7 +55,7 @@ int main(void) {
   F(skv_config, tokens_per_frame) F(skv_config, capacity) F(skv_config, max_frames) F(skv_config, dtype)
   F(skv_config, softmax_scale) F(skv_config, pos_offset) F(skv_config, policy) F(skv_config, max_decode_tokens)
   F(skv_config, rope) F(skv_config, rope_theta) F(skv_config, rope_factor) F(skv_config, rope_orig_max)
-  F(skv_config, split_refresh)
+  F(skv_config, split_refresh) F(skv_config, key_split_mode)
   F(skv_state_view_t, k) F(skv_state_view_t, v) F(skv_state_view_t, pos) F(skv_state_view_t, score)
   F(skv_state_view_t, size) F(skv_state_view_t, capacity) F(skv_state_view_t, frame)
   F(skv_state_view_t, pool_score) F(skv_state_view_t, pool_pos) F(skv_state_view_t, pool_size)
@@ -106,6 +106,8 @@ def _cfg(**kw):
     (dict(rope=2, rope_theta=1e4, rope_factor=0.5, rope_orig_max=4096), B.SKV_ERR_INVALID_ARG),
     (dict(rope=2, rope_theta=1e4, rope_factor=4.0, rope_orig_max=0), B.SKV_ERR_INVALID_ARG),
     (dict(split_refresh=2), B.SKV_ERR_INVALID_ARG),
+    (dict(key_split_mode=3), B.SKV_ERR_INVALID_ARG),
+    (dict(key_split_mode=-1), B.SKV_ERR_INVALID_ARG),
 ])
 def test_init_rejects_bad_configs_before_touching_the_device(lib, kw, status):
     h = ctypes.c_void_p(123)
