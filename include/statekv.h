@@ -173,7 +173,10 @@ skv_status skv_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count
  * results; nothing in it has to start at zero.  Calls that overlap on one device
  * (contexts on different streams) race on the array: serialise them.  Since the
  * array is reused by the next call, this entry point never defers a selection
- * (see skv_frame_step); it enqueues one that an earlier skv_frame_step deferred. */
+ * (see skv_frame_step); it enqueues one that an earlier skv_frame_step deferred.
+ * A captured call is one frame of one stream: its launches carry the frame's
+ * sizes and positions (and a key-split launch its exchange epoch), so a graph
+ * holding it must not be replayed as a later frame. */
 skv_status skv_frame_step_noalloc(skv_ctx* ctx, int32_t layer_begin, int32_t layer_count,
                                   const void* q, const void* k, const void* v, void* out);
 
