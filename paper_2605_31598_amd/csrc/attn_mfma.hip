@@ -38,6 +38,17 @@
 //     wholly inside the state are copied with per-lane offsets fixed once per launch.
 //   * The host plan keeps the row tiles of one (layer, KV head) on one XCD so
 //     they share K/V in that XCD's L2.
+//   * Calls too small to fill the device split the keys into ranges (key-split
+//     plans).  The statistics of all ranges of a row range are merged before
+//     sweep 2: across two launches (modes 1, 2) or in one (modes 3, 4), whose
+//     workgroups publish their ranges' statistics and wait a bounded time for
+//     each other's (device-scope stores and flags), computing any range that
+//     has not arrived.  Sweep 2 then writes the range's exact column sums and its
+//     fp32 share of O; the refresh launch adds the shares.
+//   * Instantiations: VAR 0 for everything but key-split output work; VAR 1 for
+//     a two-launch output launch and VAR 2 for the one-launch key split, which
+//     can also carry an earlier one-layer call's selection and state update
+//     (select.h) in extra workgroups after the plan's items.
 //
 // MFMA v_mfma_f32_32x32x16_bf16 (wave64) operand layout, lane l, h = l / 32:
 //   A (32x16): A[l % 32][8h .. 8h+7]   B (16x32): B[8h .. 8h+7][l % 32]
