@@ -37,16 +37,30 @@ ATTN_SOURCES = ["paper_2605_31598_amd/csrc/attn_mfma.hip", "paper_2605_31598_amd
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_mfma_vlm7b_28layer_traffic.txt")
 
 
+def _code_only(text):
+    """Source text without // comments and blank lines (a comment edit leaves the
+    kernel, and so its counters, unchanged)."""
+    out = []
+    for line in text.splitlines():
+        code = line.split("//", 1)[0].rstrip()
+        if code:
+            out.append(code)
+    return "\n".join(out)
+
+
 def attn_source_hash():
-    """Hash of what the attention kernel is built from: its source file and the
-    launch-argument struct it reads (the rest of internal.h serves other kernels)."""
+    """Hash of what the attention kernel is built from: its source file, the shared
+    selection code it includes, and the launch-argument structs it reads (the rest of
+    internal.h serves other kernels); comments excluded."""
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, ATTN_SOURCES[0]), "rb") as f:
-        h.update(f.read())
+    for name in (ATTN_SOURCES[0], "paper_2605_31598_amd/csrc/select.h"):
+        with open(os.path.join(ROOT, name), "r") as f:
+            h.update(_code_only(f.read()).encode())
     with open(os.path.join(ROOT, ATTN_SOURCES[1]), "r") as f:
         text = f.read()
-    start = text.index("struct AttnArgs {")
-    h.update(text[start:text.index("};", start) + 2].encode())
+    for struct in ("struct RefreshArgs {", "struct AttnArgs {"):
+        start = text.index(struct)
+        h.update(_code_only(text[start:text.index("};", start) + 2]).encode())
     return h.hexdigest()[:16]
 
 
