@@ -364,6 +364,60 @@ def large_bench(stream, name="vlm72b_80layer", timed=16, kv_heads=None):
     return res
 
 
+def t259_line(stream, timed=64, warm=64, F=24):
+    """The 7B-shaped 28-layer stack at 259 tokens per frame (the token count of the
+    paper's InternVL3 setting; 7 x 259 = 1813 query rows per KV head, not a multiple of
+    the 32-row wave blocks), capacity 2048, i.i.d. N(0,1) bf16 inputs generated on the
+    device (F frames, cycled): the state fills, `warm` state-full frames run untimed,
+    then `timed` frames are timed by HIP events with no host wait in between."""
+    from paper_2605_31598_amd import FrameStepper
+    from workloads import CONFIGS
+    from workloads import device as wdev
+    from workloads import generate as gen
+    import torch
+
+    wl = CONFIGS["vlm7b_28layer"].with_(name="vlm7b_28layer_t259", tokens_per_frame=259)
+    L, Hq, Hkv, T, d = wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.tokens_per_frame, wl.head_dim
+    fill = -(-wl.capacity // T)
+    q = torch.empty((F, L, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    k = torch.empty((F, L, Hkv, T, d), dtype=torch.bfloat16, device="cuda")
+    v = torch.empty_like(k)
+    for t, tid in ((q, gen.TENSOR_Q), (k, gen.TENSOR_K), (v, gen.TENSOR_V)):
+        wdev.fill_iid(t, [gen.stream_key(wl.seed, l, f, tid) for f in range(F) for l in range(L)], "bf16")
+    out = torch.empty((L, Hq, T, d), dtype=torch.bfloat16, device="cuda")
+    st = FrameStepper.from_workload(wl, max_frames=fill + warm + timed, stream=stream)
+    try:
+        for n in range(fill + warm):
+            st.step(q[n % F], k[n % F], v[n % F], out)
+        st.timing_start(timed)  # the host creates the events while the device runs the frames above
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for n in range(fill + warm, fill + warm + timed):
+            st.step(q[n % F], k[n % F], v[n % F], out)
+        b.record()
+        b.synchronize()
+        gpu_s = a.elapsed_time(b) * 1e-3
+        stages = st.timing_stop(timed).astype(np.float64)
+    finally:
+        st.close()
+    del q, k, v
+    att = stages[:, 0]
+    alg = attention_flops(wl, wl.capacity)
+    exe = executed_mfma_flops(wl, wl.capacity)
+    frame_ms = stages.sum(axis=1)
+    res = {"workload": wl.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "tokens_per_frame": T,
+           "capacity": wl.capacity, "inputs": "i.i.d. N(0,1) bf16, generated in HBM",
+           "timed_frames_at_state_full": timed, "frames_per_s": round(timed / gpu_s, 2),
+           "ms_per_frame": round(1e3 * gpu_s / timed, 4), "attention_ms": round(float(att.mean()), 4),
+           "refresh_ms": round(float(stages[:, 1].mean()), 4),
+           "attention_tflops": round(alg / (att.mean() * 1e-3) / 1e12, 1),
+           "attention_frac_of_bf16_peak": round(alg / (att.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "executed_mfma_frac": round(exe / (att.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "flatness_max_dev": round(float(np.max(np.abs(frame_ms / np.median(frame_ms) - 1.0))), 4)}
+    print(f"[bench] {wl.name}: {res['frames_per_s']} frames/s at state full", file=sys.stderr, flush=True)
+    return res
+
+
 def copy_bandwidth(n_bytes=1 << 30, reps=5):
     """Read + write GB/s of the runtime's device-to-device copy of 1 GiB: the practical
     streaming rate the refresh launch's GB/s is set against."""
@@ -863,6 +917,7 @@ def main():
         result["vlm7b_1layer"] = single_layer_line("vlm7b_1layer", stream, heat_frames=768)
         result["stress_1layer"] = single_layer_line("stress_1layer", stream, heat_frames=128)
         result["diagnostics"] = diagnostics_bench(stream)
+        result["vlm7b_t259"] = t259_line(stream)
         result["vlm72b"] = large_bench(stream)
         result["vlm72b_shard8"] = large_bench(stream, kv_heads=1)
         result["hbm"]["copy_GBps"] = copy_bandwidth()

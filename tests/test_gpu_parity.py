@@ -165,6 +165,21 @@ def test_full_size_one_layer_per_call_on_forced_full_state(name, layers, frame):
     say(f"{name} frames {frame}-{frame + 1}, one layer per call: {s}")
 
 
+T259 = CONFIGS["vlm7b_28layer"].with_(name="vlm7b_28layer_t259", tokens_per_frame=259)
+
+
+@pytest.mark.parametrize("per_layer", [False, True], ids=["whole_stack", "one_layer_per_call"])
+def test_259_tokens_per_frame_on_forced_full_state(per_layer):
+    """The 7B-shaped stack at 259 tokens per frame (the paper's InternVL3 setting): 1813
+    query rows per KV head, not a multiple of the 32-row wave blocks.  One layer per call
+    splits the keys 8 ways (256 workgroups, as many as the device has compute units)."""
+    wl, frame = T259, 12
+    layers = [0, 27]
+    forced = {l: recent_state(wl, l, frame) for l in layers}
+    s = run_tracking(wl, 2, layers, start_frame=frame, forced=forced, per_layer=per_layer)
+    say(f"{wl.name} frames {frame}-{frame + 1}{', one layer per call' if per_layer else ''}: {s}")
+
+
 def test_stress_ties_resolved_by_position():
     """Stress keys on the most recent state entering frame 15: exact duplicate rows give
     bit-equal scores on both sides, and in at least one KV head the tied entries straddle
