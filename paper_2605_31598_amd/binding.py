@@ -41,7 +41,7 @@ STAGES = ("attention", "refresh", "state_update", "append")
 EXPORTS = (
     "skv_init", "skv_frame_step", "skv_frame_step_noalloc", "skv_decode_step", "skv_state_view",
     "skv_decode_cache_view", "skv_reset", "skv_seek",
-    "skv_timing_start", "skv_timing_stop", "skv_destroy", "skv_status_string", "skv_last_error",
+    "skv_timing_start", "skv_timing_stride", "skv_timing_stop", "skv_destroy", "skv_status_string", "skv_last_error",
 )
 
 
@@ -106,6 +106,7 @@ def load_library(path: str = LIB_PATH):
     lib.skv_reset.argtypes = [ctypes.c_void_p]
     lib.skv_seek.argtypes = [ctypes.c_void_p, ctypes.c_int64]
     lib.skv_timing_start.argtypes = [ctypes.c_void_p, ctypes.c_int32]
+    lib.skv_timing_stride.argtypes = [ctypes.c_void_p, ctypes.c_int32]
     lib.skv_timing_stop.argtypes = [ctypes.c_void_p, P(ctypes.c_int32), P(ctypes.c_float), ctypes.c_int32]
     lib.skv_destroy.argtypes = [ctypes.c_void_p]
     lib.skv_destroy.restype = None
@@ -115,7 +116,7 @@ def load_library(path: str = LIB_PATH):
     lib.skv_last_error.restype = ctypes.c_char_p
     for name in ("skv_init", "skv_frame_step", "skv_frame_step_noalloc", "skv_decode_step", "skv_state_view",
                  "skv_decode_cache_view", "skv_reset",
-                 "skv_seek", "skv_timing_start", "skv_timing_stop"):
+                 "skv_seek", "skv_timing_start", "skv_timing_stride", "skv_timing_stop"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -193,6 +194,10 @@ def skv_seek(ctx: int, frame: int) -> None:
 
 def skv_timing_start(ctx: int, max_steps: int) -> None:
     _check(load_library().skv_timing_start(ctypes.c_void_p(ctx), max_steps), "skv_timing_start")
+
+
+def skv_timing_stride(ctx: int, stride: int) -> None:
+    _check(load_library().skv_timing_stride(ctypes.c_void_p(ctx), stride), "skv_timing_stride")
 
 
 def skv_timing_stop(ctx: int, max_steps: int) -> np.ndarray:

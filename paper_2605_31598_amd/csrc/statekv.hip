@@ -117,6 +117,8 @@ struct skv_ctx {
   std::vector<hipEvent_t> events;  // (SKV_N_STAGES + 1) per recorded step
   std::vector<uint8_t> recorded;   // per recorded step: bit i set when events[i] was recorded
   int timing_max = 0, timing_n = 0;
+  int timing_stride = 1;     // record every timing_stride-th step
+  int64_t timing_seen = 0;   // steps since skv_timing_start
 };
 
 namespace {
@@ -467,8 +469,12 @@ skv_status check_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_cou
   return SKV_OK;
 }
 
-// Scratch bytes a frame step of layer_count layers needs (each buffer 256-byte aligned),
-// and the buffers carved from `base` when base is not null.
+// Whether this step records timing events (and takes the next event slots).
+bool take_timing(skv_ctx* ctx) {
+  if (ctx->timing_n >= ctx->timing_max) return false;
+  return ctx->timing_seen++ % ctx->timing_stride == 0;
+}
+
 // Enqueues, as a launch of its own, the selection a one-layer call left for a
 // later output launch (if any).
 hipError_t flush_pending(skv_ctx* ctx) {
@@ -477,6 +483,8 @@ hipError_t flush_pending(skv_ctx* ctx) {
   return skv::launch_refresh(ctx->pend_ra, ctx->stream);
 }
 
+// Scratch bytes a frame step of layer_count layers needs (each buffer 256-byte aligned),
+// and the buffers carved from `base` when base is not null.
 size_t carve_scratch(const skv_ctx* ctx, int32_t layer_count, char* base, StepScratch* sc) {
   const skv_config& c = ctx->cfg;
   const size_t LH = static_cast<size_t>(layer_count) * c.n_kv_heads;
@@ -518,7 +526,7 @@ skv_status enqueue_frame_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_c
   const size_t lh0 = static_cast<size_t>(layer_begin) * Hkv;
   const size_t rb = ctx->row_bytes;
 
-  const bool timing = ctx->timing_n < ctx->timing_max;
+  const bool timing = take_timing(ctx);
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
   uint8_t* rec = timing ? &ctx->recorded[static_cast<size_t>(ctx->timing_n)] : nullptr;
   if (timing) *rec = 0;
@@ -815,7 +823,7 @@ skv_status skv_decode_step(skv_ctx* ctx, int32_t layer_begin, int32_t layer_coun
   ra.select = false;  // append only
   ra.append = true;
 
-  const bool timing = ctx->timing_n < ctx->timing_max;
+  const bool timing = take_timing(ctx);
   hipEvent_t* ev = timing ? &ctx->events[static_cast<size_t>(ctx->timing_n) * (SKV_N_STAGES + 1)] : nullptr;
   uint8_t* rec = timing ? &ctx->recorded[static_cast<size_t>(ctx->timing_n)] : nullptr;
   if (timing) *rec = 0;
@@ -933,6 +941,14 @@ skv_status skv_timing_start(skv_ctx* ctx, int32_t max_steps) {
   }
   ctx->timing_max = max_steps;
   ctx->timing_n = 0;
+  ctx->timing_stride = 1;
+  ctx->timing_seen = 0;
+  return SKV_OK;
+}
+
+skv_status skv_timing_stride(skv_ctx* ctx, int32_t stride) {
+  if (ctx == nullptr || stride < 1) return fail(SKV_ERR_INVALID_ARG, "bad timing stride");
+  ctx->timing_stride = stride;
   return SKV_OK;
 }
 

@@ -178,8 +178,12 @@ class FrameStepper:
                 B.copy_to_device(base + g * M * d * self.elem, np.ascontiguousarray(arr[g], dtype=self.np_dtype))
 
     # ------------------------------------------------------------ timing
-    def timing_start(self, max_steps):
+    def timing_start(self, max_steps, stride=1):
+        """Record stage events on the next max_steps steps, or with stride > 1 on every
+        stride-th step (the first, stride + 1-th, ...) until max_steps are recorded."""
         B.skv_timing_start(self.ctx, max_steps)
+        if stride != 1:
+            B.skv_timing_stride(self.ctx, stride)
 
     def timing_stop(self, max_steps):
         return B.skv_timing_stop(self.ctx, max_steps)

@@ -128,6 +128,7 @@ def test_null_arguments(lib):
     assert lib.skv_reset(None) == B.SKV_ERR_INVALID_ARG
     assert lib.skv_seek(None, 0) == B.SKV_ERR_INVALID_ARG
     assert lib.skv_timing_start(None, 4) == B.SKV_ERR_INVALID_ARG
+    assert lib.skv_timing_stride(None, 8) == B.SKV_ERR_INVALID_ARG
     lib.skv_destroy(None)
 
 

@@ -368,3 +368,28 @@ def test_split_refresh_launches_match_the_fused_launch(name, L, Hq, Hkv, d, T, B
     finally:
         a.close()
         b.close()
+
+
+def test_timing_stride_records_every_nth_step():
+    """With a timing stride of 3, ten frame steps record events on steps 0, 3, 6 and 9
+    only (four rows, each with a positive attention and refresh time); a limit of two
+    recorded steps stops after steps 0 and 3; the outputs are those of an untimed context."""
+    wl = WorkloadConfig("stride", 2, 8, 2, 64, 40, 10, 64, "bf16", "iid", 4242)
+    L, Hq, T, d = wl.n_layers, wl.n_q_heads, wl.tokens_per_frame, wl.head_dim
+    a, b, c = (FrameStepper.from_workload(wl) for _ in range(3))
+    try:
+        oa, ob, oc = (torch.empty((L, Hq, T, d), dtype=torch.bfloat16, device="cuda") for _ in range(3))
+        a.timing_start(8, stride=3)
+        b.timing_start(2, stride=3)
+        for n in range(wl.n_frames):
+            q, k, v, _ = frame_tensors(wl, n, list(range(L)))
+            for s, o in ((a, oa), (b, ob), (c, oc)):
+                s.step(q, k, v, o)
+            assert torch.equal(oa.view(torch.int16), oc.view(torch.int16)), f"frame {n}"
+            assert torch.equal(ob.view(torch.int16), oc.view(torch.int16)), f"frame {n}"
+        ta, tb = a.timing_stop(8), b.timing_stop(8)
+        assert ta.shape[0] == 4 and tb.shape[0] == 2
+        assert np.all(ta[:, :2] > 0.0) and np.all(tb[:, :2] > 0.0)
+    finally:
+        for s in (a, b, c):
+            s.close()
