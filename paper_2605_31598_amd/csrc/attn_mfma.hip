@@ -282,20 +282,21 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KROW = (D + kPadK) / 8, VROW = (D + kPadV) / 8;  // 16-byte slots per padded row
   constexpr int KINS = kKT * KROW / 64, VINS = kKT * VROW / 64;  // instructions per tile
   static_assert(KINS * 64 == kKT * KROW && VINS * 64 == kKT * VROW, "whole instructions per tile");
-  constexpr int KIT = (KINS + kWaves - 1) / kWaves, VIT = (VINS + kWaves - 1) / kWaves;
-  int koff[KIT], voff[VIT];  // element offset of this lane's slot inside a tile (rows of D)
-#pragma unroll
-  for (int it = 0; it < KIT; ++it) {
-    const int q = (it * kWaves + wave) * 64 + lane;
-    const int ch = q % KROW;
-    koff[it] = (q / KROW) * D + (ch < KCH ? ch : 0) * 8;
-  }
-#pragma unroll
-  for (int it = 0; it < VIT; ++it) {
-    const int q = (it * kWaves + wave) * 64 + lane;
-    const int ch = q % VROW;
-    voff[it] = (q / VROW) * D + (ch < KCH ? ch : 0) * 8;
-  }
+  // Only waves 0-3 issue the copies.  Waves w and w + 4 of a workgroup share a
+  // SIMD, and the younger one (w + 4) finishes a tile last; copy instructions
+  // issued at a tile's start hold a wave until the load unit takes them, so they
+  // go to the wave of each pair that would otherwise wait at the tile barrier.
+  constexpr int kDW = kWaves / 2;
+  constexpr int KIT = (KINS + kDW - 1) / kDW, VIT = (VINS + kDW - 1) / kDW;
+  const bool dma_wave = wave < kDW;
+  // element offset of slot q of a tile (rows of D), computed at the copy
+  auto slot_off = [&](int q, auto rowc) -> int {
+    constexpr int ROW = decltype(rowc)::value;
+    const int ch = q % ROW;
+    return (q / ROW) * D + (ch < KCH ? ch : 0) * 8;
+  };
+  auto koff_at = [&](int it) { return slot_off((it * kDW + wave) * 64 + lane, std::integral_constant<int, KROW>{}); };
+  auto voff_at = [&](int it) { return slot_off((it * kDW + wave) * 64 + lane, std::integral_constant<int, VROW>{}); };
   auto dma_one = [&](const uint16_t* src, uint16_t* dst_tile, int ins) {
     __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
                                      (void __attribute__((address_space(3)))*)(reinterpret_cast<char*>(dst_tile) + ins * 1024),
@@ -306,17 +307,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     j = j < n_keys ? j : n_keys - 1;
     return j < S ? st + static_cast<size_t>(j) * D : fr + static_cast<size_t>(j - S) * D;
   };
-  auto dma_tile = [&](int t, int b, bool with_v, auto pure) {
+  auto dma_tile = [&](int t, int b, bool with_v, auto pure) __attribute__((always_inline)) {
+    if (!dma_wave) return;
 #pragma unroll
     for (int it = 0; it < KIT; ++it) {
-      const int ins = it * kWaves + wave;
+      const int ins = it * kDW + wave;
       if (ins < KINS) {
         const uint16_t* src;
         if constexpr (decltype(pure)::value) {
-          src = kst + static_cast<size_t>(t) * kKT * D + koff[it];
+          src = kst + static_cast<size_t>(t) * kKT * D + koff_at(it);
         } else {
-          const int r = koff[it] / D;
-          src = key_src(kst, kfr, t * kKT + r) + (koff[it] - r * D);
+          const int ko = koff_at(it), r = ko / D;
+          src = key_src(kst, kfr, t * kKT + r) + (ko - r * D);
         }
         dma_one(src, &sm.k[b][0][0], ins);
       }
@@ -324,14 +326,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (!with_v) return;
 #pragma unroll
     for (int it = 0; it < VIT; ++it) {
-      const int ins = it * kWaves + wave;
+      const int ins = it * kDW + wave;
       if (ins < VINS) {
         const uint16_t* src;
         if constexpr (decltype(pure)::value) {
-          src = vst + static_cast<size_t>(t) * kKT * D + voff[it];
+          src = vst + static_cast<size_t>(t) * kKT * D + voff_at(it);
         } else {
-          const int r = voff[it] / D;
-          src = key_src(vst, vfr, t * kKT + r) + (voff[it] - r * D);
+          const int vo = voff_at(it), r = vo / D;
+          src = key_src(vst, vfr, t * kKT + r) + (vo - r * D);
         }
         dma_one(src, &sm.v[b][0][0], ins);
       }
