@@ -282,21 +282,25 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
   constexpr int KROW = (D + kPadK) / 8, VROW = (D + kPadV) / 8;  // 16-byte slots per padded row
   constexpr int KINS = kKT * KROW / 64, VINS = kKT * VROW / 64;  // instructions per tile
   static_assert(KINS * 64 == kKT * KROW && VINS * 64 == kKT * VROW, "whole instructions per tile");
-  // Only waves 0-3 issue the copies.  Waves w and w + 4 of a workgroup share a
-  // SIMD, and the younger one (w + 4) finishes a tile last; copy instructions
-  // issued at a tile's start hold a wave until the load unit takes them, so they
-  // go to the wave of each pair that would otherwise wait at the tile barrier.
+  // The copies of the next tile, issued while the current one is computed, come
+  // from waves 0-3 only: waves w and w + 4 of a workgroup share a SIMD, and the
+  // younger one (w + 4) finishes a tile last; copy instructions issued at a
+  // tile's start hold a wave until the load unit takes them, so they go to the
+  // wave of each pair that would otherwise wait at the tile barrier.  A copy the
+  // whole workgroup waits for (a range's first tile) is shared by all eight
+  // waves: waves 4-7 take every second instruction of waves 0-3's schedule.
   constexpr int kDW = kWaves / 2;
   constexpr int KIT = (KINS + kDW - 1) / kDW, VIT = (VINS + kDW - 1) / kDW;
-  const bool dma_wave = wave < kDW;
+  const bool upper = wave >= kDW;
+  const int dw = wave & (kDW - 1);  // position in the schedule of waves 0-3
   // element offset of slot q of a tile (rows of D), computed at the copy
   auto slot_off = [&](int q, auto rowc) -> int {
     constexpr int ROW = decltype(rowc)::value;
     const int ch = q % ROW;
     return (q / ROW) * D + (ch < KCH ? ch : 0) * 8;
   };
-  auto koff_at = [&](int it) { return slot_off((it * kDW + wave) * 64 + lane, std::integral_constant<int, KROW>{}); };
-  auto voff_at = [&](int it) { return slot_off((it * kDW + wave) * 64 + lane, std::integral_constant<int, VROW>{}); };
+  auto koff_at = [&](int it) { return slot_off((it * kDW + dw) * 64 + lane, std::integral_constant<int, KROW>{}); };
+  auto voff_at = [&](int it) { return slot_off((it * kDW + dw) * 64 + lane, std::integral_constant<int, VROW>{}); };
   auto dma_one = [&](const uint16_t* src, uint16_t* dst_tile, int ins) {
     __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
                                      (void __attribute__((address_space(3)))*)(reinterpret_cast<char*>(dst_tile) + ins * 1024),
@@ -307,12 +311,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     j = j < n_keys ? j : n_keys - 1;
     return j < S ? st + static_cast<size_t>(j) * D : fr + static_cast<size_t>(j - S) * D;
   };
-  auto dma_tile = [&](int t, int b, bool with_v, auto pure) __attribute__((always_inline)) {
-    if (!dma_wave) return;
+  // all: every wave takes part (else waves 0-3 issue everything)
+  auto dma_tile = [&](int t, int b, bool with_v, auto pure, bool all) __attribute__((always_inline)) {
+    if (!all && upper) return;
 #pragma unroll
     for (int it = 0; it < KIT; ++it) {
-      const int ins = it * kDW + wave;
-      if (ins < KINS) {
+      const int ins = it * kDW + dw;
+      if (ins < KINS && (!all || ((it & 1) != 0) == upper)) {
         const uint16_t* src;
         if constexpr (decltype(pure)::value) {
           src = kst + static_cast<size_t>(t) * kKT * D + koff_at(it);
@@ -326,8 +331,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     if (!with_v) return;
 #pragma unroll
     for (int it = 0; it < VIT; ++it) {
-      const int ins = it * kDW + wave;
-      if (ins < VINS) {
+      const int ins = it * kDW + dw;
+      if (ins < VINS && (!all || ((it & 1) != 0) == upper)) {
         const uint16_t* src;
         if constexpr (decltype(pure)::value) {
           src = vst + static_cast<size_t>(t) * kKT * D + voff_at(it);
@@ -381,7 +386,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     const uint32_t kaddr = lds_addr(&sm.k[b][key0 + l32][h * 8]);
     u32x4 kop[KS];
     if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
-    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, false, pure_next);
+    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, false, pure_next, false);
     // masked tiles: blocks whose first key is past the wave's limit (a suffix) are skipped
     const int first = t * kKT + key0;
     const int na = !decltype(masked)::value ? NB : wlim < first ? 0 : min(NB, (wlim - first) / 32 + 1);
@@ -465,7 +470,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     auto row_stats = [&]() {
       m = -1e30f;
       l = 0.f;
-      if (kt0 < kt1) dma_tile(kt0, kt0 & 1, false, std::false_type{});
+      if (kt0 < kt1) dma_tile(kt0, kt0 & 1, false, std::false_type{}, true);
       dma_wait();
       __syncthreads();
       if (split)
@@ -522,7 +527,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
       publish(ks);
       __syncthreads();  // every wave's stores have completed; the tile buffers are free
       // sweep 2's first tile is copied while the workgroup waits for the others
-      if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
+      if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{}, true);
       const unsigned all = (1u << a.n_ks) - 1u;
       unsigned* shared_mask = reinterpret_cast<unsigned*>(&sm.il[0][0]);  // free until the epilogue
       if (tid == 0) {
@@ -558,7 +563,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
       }
       kt0 = range_lo(ks);
       kt1 = range_lo(ks + 1);
-      if (refill && kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
+      if (refill && kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{}, true);
       __syncthreads();  // the ranges computed here are in `stats` before anyone reads them
       // merge every range's statistics in split order (as the output launch of
       // the two-launch scheme does)
@@ -645,7 +650,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     const uint32_t vaddr = lds_addr(&sm.v[b][key0 + tr_row][tr_col]);
     const int first = t * kKT + key0;
     const int na = wlim < first ? 0 : min(NB, (wlim - first) / 32 + 1);
-    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, true, std::false_type{});
+    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, true, std::false_type{}, false);
     if (active) {
       static_for<NB>([&](auto kbc) {
         constexpr int KB = decltype(kbc)::value;
@@ -697,7 +702,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     const uint32_t vaddr = lds_addr(&sm.v[b][key0 + tr_row][tr_col]);
     u32x4 kop[KS];
     if (active) issue_k(std::integral_constant<int, 0>{}, kaddr, kop);
-    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, true, pure_next);
+    if (t + 1 < kt1) dma_tile(t + 1, b ^ 1, true, pure_next, false);
     if (active) {
       // Software pipeline over the tile's blocks: block kb + 1's K Q^T MFMAs are
       // issued interleaved with block kb's exponentials, block kb's PV MFMAs with
@@ -773,7 +778,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_mfma_kernel(AttnArgs a) {
     for (int t = kt0 > first_masked ? kt0 : first_masked; t < kt1; ++t) sweep2_masked_tile(t, nbc);
   };
   if constexpr (VAR != 2) {  // a fused key split issued this copy before its wait
-    if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{});
+    if (kt0 < kt1) dma_tile(kt0, kt0 & 1, true, std::false_type{}, true);
   }
   dma_wait();
   __syncthreads();
