@@ -33,6 +33,10 @@ struct SelectShared {
   uint32_t wave_total[kSelectThreads / 64];  // admit/evict scan
   int digit[2], remaining[2];           // one slot per pass parity
   uint32_t count[2];
+  uint32_t cand[64];                    // keys of a small final bin, ranked directly
+  int n_cand;
+  uint32_t res_value;
+  int res_need, res_equal;
   int32_t admit_src[kLdsAdmit];  // frame token of the a-th admitted candidate
   int32_t admit_dst[kLdsAdmit];  // state slot it goes to
 };
@@ -96,6 +100,7 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n_waves = blockDim.x >> 6;
   for (int i = tid; i < 2 * 256; i += blockDim.x) sh.hist[i >> 8][i & 255] = 0u;
+  if (tid == 0) sh.n_cand = 0;
   uint32_t lo = 0xFFFFFFFFu, hi = 0u;
   int cnt = 0;
   for (int j = tid; j < n; j += blockDim.x) {
@@ -166,6 +171,37 @@ __device__ RadixResult radix_select(int n, int rank, KeyFn key, ActiveFn active,
     prefix |= static_cast<uint32_t>(sh.digit[par]) << shift;
     remaining = sh.remaining[par];
     equal = static_cast<int>(sh.count[par]);
+    if (shift > 0 && equal <= 64) {
+      // Few keys share the prefix: instead of the remaining passes, gather them
+      // and let one wave rank them (the same value, count needed and count equal).
+      const uint32_t decided = ~((1u << shift) - 1u);
+      for (int j = tid; j < n; j += blockDim.x) {
+        if (!active(j)) continue;
+        const uint32_t k = key(j);
+        if ((k & decided) == prefix) sh.cand[atomicAdd(&sh.n_cand, 1)] = k;
+      }
+      __syncthreads();
+      if (wave == 0) {
+        const int nc = sh.n_cand;  // = equal
+        const uint32_t mine = lane < nc ? sh.cand[lane] : 0u;
+        int above = 0, same = 0;
+        for (int i = 0; i < nc; ++i) {
+          const uint32_t o = sh.cand[i];
+          above += o > mine ? 1 : 0;
+          same += o == mine ? 1 : 0;
+        }
+        // the lanes holding the remaining-th largest key (equal keys agree); the lowest writes
+        const bool hit = lane < nc && above < remaining && remaining <= above + same;
+        const uint64_t hits = __ballot(hit);
+        if (hit && lane == __ffsll(static_cast<long long>(hits)) - 1) {
+          sh.res_value = mine;
+          sh.res_need = remaining - above;
+          sh.res_equal = same;
+        }
+      }
+      __syncthreads();
+      return {sh.res_value, sh.res_need, sh.res_equal};
+    }
     for (int i = tid; i < 256; i += blockDim.x) hist[i] = 0u;  // for pass p + 2
   }
   return {prefix, remaining, equal};
