@@ -20,7 +20,9 @@
 //   * Keys stream through LDS in tiles of 128 (four 32-key blocks), double
 //     buffered, K and V both row-major with padded rows.  The load unit copies
 //     the next tile global -> LDS (global_load_lds) while the current one is
-//     computed, with no registers or LDS store instructions.  Operand reads from
+//     computed, with no registers or LDS store instructions; those copies are
+//     issued by the first wave of each SIMD (waves 0-3), whose partner sets the
+//     tile's pace, and a range's first tile by all eight.  Operand reads from
 //     LDS are issued ahead as inline assembly with explicit waits, and waves
 //     raise their priority while issuing MFMAs.
 //   * Sweep 2 is software-pipelined over the blocks of a tile: block kb + 1's
@@ -35,7 +37,8 @@
 //   * Tiles that contain frame keys (the only ones with masked entries) run in a
 //     separate loop, keeping mask code off the common path; there a wave skips the
 //     32-key blocks that lie wholly past the causal limit of all its rows.  Tiles
-//     wholly inside the state are copied with per-lane offsets fixed once per launch.
+//     wholly inside the state are copied without the per-row clamping to the
+//     last key.
 //   * The host plan keeps the row tiles of one (layer, KV head) on one XCD so
 //     they share K/V in that XCD's L2.
 //   * Calls too small to fill the device split the keys into ranges (key-split
