@@ -728,6 +728,20 @@ def oracle_timings(budget_s=20.0):
     return res
 
 
+def sampled_frames(recorded, stride):
+    """The steps that record stage events under a timing stride: for each stream of
+    `recorded` ((stream, frame) per step, in run order), the indices into `recorded` of
+    that stream's 1st, (stride + 1)-th, (2 stride + 1)-th, ... step, as the library
+    picks them (skv_timing_stride counts each context's steps from skv_timing_start)."""
+    seen, out = {}, {}
+    for g, (s, _) in enumerate(recorded):
+        j = seen.get(s, 0)
+        if j % stride == 0:
+            out.setdefault(s, []).append(g)
+        seen[s] = j + 1
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -825,9 +839,7 @@ def main():
     recorded = slots[:args.warmup + args.steps]
     used = sorted({i for i, _ in recorded})
     stride = max(1, args.event_stride) if calls == 1 else 1
-    # global indices (into recorded) of the frames whose events each stream keeps
-    sampled = {i: [g for j, g in enumerate(g for g, (s, _) in enumerate(recorded) if s == i) if j % stride == 0]
-               for i in used}
+    sampled = sampled_frames(recorded, stride)
     for i in used:
         streams[i].timing_start(calls * len(sampled[i]), stride=stride)
     heater = Heater(wl, q_all, k_all, v_all, out, stream)
